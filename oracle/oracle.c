@@ -1,0 +1,236 @@
+/*
+ * oracle.c -- plain, slow, fp64 CPU reference for gated-delta-rule (GDN)
+ * speculative verification of draft chains/trees and accepted-path commit.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test-suite, the package smoke check and
+ * the CPU-baseline leg of the benchmark may load this library.  The product
+ * path (the HIP library) never links or calls it, and this file shares no
+ * code, header, table or helper with it.
+ *
+ * What it computes (SpecLA, arXiv 2607.16673):
+ *   - The GDN recurrent step with decay alpha and delta-rule strength beta,
+ *         S' = alpha * S (I - beta k k^T) + beta v k^T ,   o = S' q,
+ *     i.e. the gated form of the minimal update of Eq. (state-update) in
+ *     §2.2, with GDN named as the target layer there.  The state is held
+ *     transposed, H = S^T with shape [d_k][d_v] (v fastest), which is the
+ *     K x V_tile orientation of the tiling paragraph of §4.1; the step in
+ *     that orientation is
+ *         H' = alpha * (H - beta k (k^T H)) + beta k v^T ,   o = H'^T q.
+ *   - Verification (§4, tree mask of §4.2): every draft node j is evaluated
+ *     on its own root path P(j) -- its ancestors, root first, then j -- so
+ *     that updates flow only along ancestor paths and never between
+ *     siblings.  The output of node j is read after node j's own update
+ *     (a chain of length one is exactly one autoregressive decode step).
+ *     This is written as the plain definition: for each node the committed
+ *     state is copied and the steps of its root path are applied one by one.
+ *     No prefix sharing, no factorisation.
+ *   - Commit (§5.1 "state recovery", §5.2): the durable state after
+ *     accepting the path a_1..a_A is the state after decoding those tokens
+ *     one at a time, starting from the committed state.
+ *   - Topology (§4.2 tree mask, §7 parent array): depth, inclusive
+ *     ancestor bit masks, child counts and a DFS pre-order, computed by the
+ *     definition (following parent pointers node by node).
+ *
+ * Units are (batch b, head h); they are independent and are distributed
+ * over OpenMP threads when the library is built with -fopenmp.  Within a
+ * unit nothing is blocked, fused or reordered.
+ *
+ * Layouts (all row-major, contiguous):
+ *   state  [B][H][dk][dv]        q, k [B][n][H][dk]      v, out [B][n][H][dv]
+ *   alpha, beta [B][n][H]        parent [B][n]           path [B][path_stride]
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define OR_OK 0
+#define OR_ERR_SHAPE (-2)
+#define OR_ERR_TOPOLOGY (-4)
+#define OR_ERR_PATH (-5)
+#define OR_MAX_NODES 64
+
+int oracle_num_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
+}
+
+/* One GDN step on H = S^T ([dk][dv]).  kH is caller scratch of length dv.
+ *   kH[c]   = sum_i k[i] H[i][c]                       (the row k^T H)
+ *   H[i][c] = alpha*(H[i][c] - beta*k[i]*kH[c]) + beta*k[i]*v[c]          */
+void oracle_gdn_step(int dk, int dv, double *H, const double *k, const double *v,
+                     double alpha, double beta, double *kH) {
+  for (int c = 0; c < dv; ++c) {
+    double s = 0.0;
+    for (int i = 0; i < dk; ++i) s += k[i] * H[(size_t)i * dv + c];
+    kH[c] = s;
+  }
+  for (int i = 0; i < dk; ++i)
+    for (int c = 0; c < dv; ++c) {
+      double h = H[(size_t)i * dv + c];
+      H[(size_t)i * dv + c] = alpha * (h - beta * k[i] * kH[c]) + beta * k[i] * v[c];
+    }
+}
+
+/* o = H^T q  (= S q). */
+void oracle_readout(int dk, int dv, const double *H, const double *q, double *o) {
+  for (int c = 0; c < dv; ++c) {
+    double s = 0.0;
+    for (int i = 0; i < dk; ++i) s += H[(size_t)i * dv + c] * q[i];
+    o[c] = s;
+  }
+}
+
+/* A parent array is valid when every node's parent is -1 (a child of the
+ * committed state) or an earlier node: the draft is in topological order
+ * (§4.2).  Returns OR_OK or OR_ERR_TOPOLOGY. */
+int oracle_check_parent(const int32_t *parent, int n) {
+  if (n < 1 || n > OR_MAX_NODES) return OR_ERR_SHAPE;
+  for (int j = 0; j < n; ++j)
+    if (parent[j] < -1 || parent[j] >= j) return OR_ERR_TOPOLOGY;
+  return OR_OK;
+}
+
+/* Root path of node j, root first, j last.  Returns its length. */
+int oracle_root_path(const int32_t *parent, int n, int j, int32_t *path) {
+  int32_t rev[OR_MAX_NODES];
+  int len = 0;
+  for (int a = j; a != -1; a = parent[a]) {
+    if (a < 0 || a >= n || len >= n) return -1;
+    rev[len++] = a;
+  }
+  for (int t = 0; t < len; ++t) path[t] = rev[len - 1 - t];
+  return len;
+}
+
+/* DFS pre-order: roots in ascending index, each node followed by the
+ * subtrees of its children in ascending index. */
+static void dfs_visit(const int32_t *parent, int n, int j, int32_t *order, int *pos) {
+  order[(*pos)++] = j;
+  for (int c = j + 1; c < n; ++c)
+    if (parent[c] == j) dfs_visit(parent, n, c, order, pos);
+}
+
+/* Topology table of one draft (one sequence).
+ *   depth[j]      = |P(j)| (a root has depth 1)
+ *   anc[j]        = bit a set iff a is on P(j) (j included)
+ *   n_children[j] = number of nodes whose parent is j
+ *   order         = DFS pre-order (see above)
+ *   *max_depth    = max_j depth[j]                                        */
+int oracle_topology(const int32_t *parent, int n, int32_t *depth, uint64_t *anc,
+                    int32_t *order, int32_t *n_children, int32_t *max_depth) {
+  int st = oracle_check_parent(parent, n);
+  if (st != OR_OK) return st;
+  int md = 0;
+  for (int j = 0; j < n; ++j) {
+    int d = 0;
+    uint64_t m = 0;
+    for (int a = j; a != -1; a = parent[a]) {
+      ++d;
+      m |= (uint64_t)1 << a;
+    }
+    depth[j] = d;
+    anc[j] = m;
+    if (d > md) md = d;
+    int c = 0;
+    for (int i = 0; i < n; ++i) c += (parent[i] == j);
+    n_children[j] = c;
+  }
+  int pos = 0;
+  for (int j = 0; j < n; ++j)
+    if (parent[j] == -1) dfs_visit(parent, n, j, order, &pos);
+  *max_depth = md;
+  return OR_OK;
+}
+
+/* An accepted path a_1..a_len is valid when it is a root path of the draft:
+ * parent[a_1] = -1 and parent[a_t] = a_{t-1}.  len = 0 is the empty path. */
+int oracle_validate_path(const int32_t *parent, int n, const int32_t *path, int len) {
+  if (len < 0 || len > n) return OR_ERR_PATH;
+  int prev = -1;
+  for (int t = 0; t < len; ++t) {
+    int a = path[t];
+    if (a < 0 || a >= n || parent[a] != prev) return OR_ERR_PATH;
+    prev = a;
+  }
+  return OR_OK;
+}
+
+/* Verification by definition.  For every (b, h) and node j: copy the
+ * committed state, apply the GDN steps of the nodes of P(j) root first,
+ * then read out o_j = H^T q_j.  status[b] (nullable) gets the per-sequence
+ * topology verdict; invalid sequences produce no output. */
+int oracle_verify(int B, int H, int dk, int dv, int n, const double *state,
+                  const double *q, const double *k, const double *v,
+                  const double *alpha, const double *beta, const int32_t *parent,
+                  double *out, int32_t *status) {
+  if (B < 1 || H < 1 || dk < 1 || dv < 1 || n < 1 || n > OR_MAX_NODES) return OR_ERR_SHAPE;
+  int bad = 0;
+  for (int b = 0; b < B; ++b) {
+    int st = oracle_check_parent(parent + (size_t)b * n, n);
+    if (status) status[b] = st;
+    if (st != OR_OK) bad = 1;
+  }
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b)
+    for (int h = 0; h < H; ++h) {
+      const int32_t *par = parent + (size_t)b * n;
+      if (oracle_check_parent(par, n) != OR_OK) continue;
+      double *Hw = (double *)malloc(sizeof(double) * ((size_t)dk * dv + dv));
+      double *kH = Hw + (size_t)dk * dv;
+      const double *H0 = state + ((size_t)b * H + h) * dk * dv;
+      int32_t path[OR_MAX_NODES];
+      for (int j = 0; j < n; ++j) {
+        int len = oracle_root_path(par, n, j, path);
+        memcpy(Hw, H0, sizeof(double) * (size_t)dk * dv);
+        for (int t = 0; t < len; ++t) {
+          size_t a = ((size_t)b * n + path[t]) * H + h;
+          oracle_gdn_step(dk, dv, Hw, k + a * dk, v + a * dv, alpha[a], beta[a], kH);
+        }
+        size_t jj = ((size_t)b * n + j) * H + h;
+        oracle_readout(dk, dv, Hw, q + jj * dk, out + jj * dv);
+      }
+      free(Hw);
+    }
+  return bad ? OR_ERR_TOPOLOGY : OR_OK;
+}
+
+/* Commit by definition: for every (b, h), starting from the committed
+ * state, decode the accepted tokens path[b][0..len[b]) one at a time with
+ * the GDN step, in place.  Sequences whose path is not a root path of their
+ * draft are left untouched and get OR_ERR_PATH in status[b] (nullable). */
+int oracle_commit(int B, int H, int dk, int dv, int n, double *state,
+                  const double *k, const double *v, const double *alpha,
+                  const double *beta, const int32_t *parent, const int32_t *path,
+                  int path_stride, const int32_t *len, int32_t *status) {
+  if (B < 1 || H < 1 || dk < 1 || dv < 1 || n < 1 || n > OR_MAX_NODES) return OR_ERR_SHAPE;
+  int bad = 0;
+  for (int b = 0; b < B; ++b) {
+    int st = oracle_check_parent(parent + (size_t)b * n, n);
+    if (st == OR_OK)
+      st = oracle_validate_path(parent + (size_t)b * n, n, path + (size_t)b * path_stride, len[b]);
+    if (status) status[b] = st;
+    if (st != OR_OK) bad = 1;
+  }
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int b = 0; b < B; ++b)
+    for (int h = 0; h < H; ++h) {
+      const int32_t *par = parent + (size_t)b * n;
+      const int32_t *pth = path + (size_t)b * path_stride;
+      if (oracle_check_parent(par, n) != OR_OK || oracle_validate_path(par, n, pth, len[b]) != OR_OK)
+        continue;
+      double *kH = (double *)malloc(sizeof(double) * dv);
+      double *Hs = state + ((size_t)b * H + h) * dk * dv;
+      for (int t = 0; t < len[b]; ++t) {
+        size_t a = ((size_t)b * n + pth[t]) * H + h;
+        oracle_gdn_step(dk, dv, Hs, k + a * dk, v + a * dv, alpha[a], beta[a], kH);
+      }
+      free(kH);
+    }
+  return bad ? OR_ERR_PATH : OR_OK;
+}

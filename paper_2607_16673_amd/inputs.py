@@ -1,0 +1,215 @@
+"""Seeded synthetic inputs for GDN tree/chain verification and commit.
+
+This module is shared by the tests, the smoke check and the benchmark to feed
+*both* the HIP library and the CPU oracle.  It holds the workload recipe only
+(shapes, distributions, random draft trees, accepted paths) and none of the
+verification or commit arithmetic.
+
+Workload recipe (stand-ins for the GDN-1.3B activations and recorded EAGLE
+proposal trees of the paper's evaluation, §8, which are not available):
+  * committed state S ~ N(0, 0.02^2), fp32, stored as H = S^T [dk][dv];
+  * q, k ~ N(0, 1), L2-normalised per (layer, b, node, head) in fp64, then
+    rounded (round-to-nearest-even) to the activation dtype;
+  * v ~ N(0, 1), rounded to the activation dtype;
+  * alpha = sigmoid(x), x ~ U(2, 5); beta = sigmoid(z), z ~ N(0, 1); fp32;
+  * chains: parent[j] = j - 1; trees: node 0 is the root, node i > 0 picks a
+    uniform parent among earlier nodes whose depth and child count are still
+    below the configured limits;
+  * accepted path: chains accept a uniform prefix length in [0, n]; trees
+    accept the root path of a uniformly drawn node.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+
+F32 = "f32"
+BF16 = "bf16"
+
+
+@dataclass(frozen=True)
+class Config:
+    name: str
+    index: int
+    batch: int
+    heads: int
+    d_k: int
+    d_v: int
+    n_nodes: int
+    chain: bool
+    max_depth: int
+    max_branch: int
+    dtype: str
+    layers: int
+    description: str = ""
+
+
+CONFIGS = {
+    c.name: c
+    for c in [
+        Config("tiny_chain_f32", 0, 1, 1, 64, 64, 4, True, 4, 1, F32, 1,
+               "batch 1, 1 head, dk=dv=64, chain of 4, all fp32"),
+        Config("chain8_bf16", 1, 1, 16, 128, 128, 8, True, 8, 1, BF16, 1,
+               "batch 1, 16 heads, dk=dv=128, chain of 8, bf16 q/k/v"),
+        Config("tree32_bf16", 2, 1, 16, 128, 128, 32, False, 6, 4, BF16, 1,
+               "batch 1, 16 heads, dk=dv=128, 32-node tree (depth<=6, branch<=4)"),
+        Config("batched_tree_serving", 3, 64, 16, 128, 128, 16, False, 5, 3, BF16, 24,
+               "batch 64, 16 heads, dk=dv=128, 16-node trees (depth<=5, branch<=3), 24 layers"),
+        Config("large_batch_tree64", 4, 256, 16, 128, 256, 64, False, 8, 4, BF16, 1,
+               "batch 256, 16 heads, dk=128, dv=256, 64-node trees (depth<=8, branch<=4)"),
+        Config("large_batch_chain1", 5, 256, 16, 128, 256, 1, True, 1, 1, BF16, 1,
+               "batch 256, 16 heads, dk=128, dv=256, 1-node chain (decode reference)"),
+        Config("paper_fused_shape", 6, 1, 8, 256, 256, 4, True, 4, 1, BF16, 1,
+               "batch 1, 8 heads, dk=dv=256, chain of 4 (fused commit-and-verify study shape)"),
+    ]
+}
+
+
+def config(name: str) -> Config:
+    return CONFIGS[name]
+
+
+def base_seed(cfg: Config) -> int:
+    return 1000 + cfg.index
+
+
+def _rng(*key: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([int(x) for x in key])))
+
+
+# ---------------------------------------------------------------- bf16 storage
+def bf16_bits(x) -> np.ndarray:
+    """Round fp32 values to bf16 (round to nearest, ties to even); uint16 bits."""
+    u = np.ascontiguousarray(np.asarray(x, dtype=np.float32)).view(np.uint32)
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+    return r.astype(np.uint16)
+
+
+def bf16_to_f32(bits) -> np.ndarray:
+    b = np.ascontiguousarray(np.asarray(bits, dtype=np.uint16)).astype(np.uint32)
+    return (b << np.uint32(16)).view(np.float32)
+
+
+# ---------------------------------------------------------------- topologies
+def random_tree(rng: np.random.Generator, n: int, max_depth: int, max_branch: int) -> np.ndarray:
+    """Parent array of a random draft tree; node 0 is the only root."""
+    parent = np.full(n, -1, np.int32)
+    depth = np.zeros(n, np.int64)
+    kids = np.zeros(n, np.int64)
+    depth[0] = 1
+    for i in range(1, n):
+        eligible = [a for a in range(i) if depth[a] < max_depth and kids[a] < max_branch]
+        if not eligible:
+            raise ValueError("depth/branch limits too tight for %d nodes" % n)
+        p = eligible[int(rng.integers(len(eligible)))]
+        parent[i] = p
+        depth[i] = depth[p] + 1
+        kids[p] += 1
+    return parent
+
+
+def chain(n: int) -> np.ndarray:
+    return np.arange(-1, n - 1, dtype=np.int32)
+
+
+def walk_to_root(parent: np.ndarray, j: int) -> list:
+    """Node ids from the root down to j (used to pick an accepted path)."""
+    out = []
+    a = int(j)
+    while a != -1:
+        out.append(a)
+        a = int(parent[a])
+    return out[::-1]
+
+
+# ---------------------------------------------------------------- draws
+def _normalised(rng: np.random.Generator, shape) -> np.ndarray:
+    x = rng.standard_normal(shape)  # fp64
+    x /= np.linalg.norm(x, axis=-1, keepdims=True)
+    return x
+
+
+def _to_dtype(x64: np.ndarray, dtype: str):
+    """(storage array, exact fp32 values) for the activation dtype."""
+    x32 = np.asarray(x64, dtype=np.float32)
+    if dtype == BF16:
+        bits = bf16_bits(x32)
+        return bits, bf16_to_f32(bits)
+    return x32, x32
+
+
+@dataclass
+class Round:
+    """One speculative round of one configuration (all layers)."""
+    parent: np.ndarray           # [B][n] int32
+    path: np.ndarray             # [B][n] int32, -1 padded
+    length: np.ndarray           # [B] int32
+    q: list = field(default_factory=list)      # per layer: storage array [B][n][H][dk]
+    k: list = field(default_factory=list)
+    v: list = field(default_factory=list)      # [B][n][H][dv]
+    q32: list = field(default_factory=list)    # exact fp32 values of the above
+    k32: list = field(default_factory=list)
+    v32: list = field(default_factory=list)
+    alpha: list = field(default_factory=list)  # [B][n][H] fp32
+    beta: list = field(default_factory=list)
+
+
+def draw_topology(cfg: Config, round_index: int = 0, batch: int | None = None):
+    """Parent arrays and accepted paths of one round (shared by all layers)."""
+    B = cfg.batch if batch is None else batch
+    n = cfg.n_nodes
+    rng = _rng(base_seed(cfg), round_index, 0)
+    parent = np.zeros((B, n), np.int32)
+    path = np.full((B, n), -1, np.int32)
+    length = np.zeros(B, np.int32)
+    for b in range(B):
+        if cfg.chain:
+            parent[b] = chain(n)
+        else:
+            parent[b] = random_tree(rng, n, cfg.max_depth, cfg.max_branch)
+    for b in range(B):
+        if cfg.chain:
+            A = 1 if n == 1 else int(rng.integers(0, n + 1))
+            p = list(range(A))
+        else:
+            p = walk_to_root(parent[b], int(rng.integers(0, n)))
+        path[b, :len(p)] = p
+        length[b] = len(p)
+    return parent, path, length
+
+
+def draw_layer(cfg: Config, layer: int, round_index: int = 0, batch: int | None = None):
+    """q, k, v, alpha, beta of one layer of one round."""
+    B = cfg.batch if batch is None else batch
+    n, H, dk, dv = cfg.n_nodes, cfg.heads, cfg.d_k, cfg.d_v
+    rng = _rng(base_seed(cfg), round_index, 1, layer)
+    q64 = _normalised(rng, (B, n, H, dk))
+    k64 = _normalised(rng, (B, n, H, dk))
+    v64 = rng.standard_normal((B, n, H, dv))
+    alpha = (1.0 / (1.0 + np.exp(-rng.uniform(2.0, 5.0, (B, n, H))))).astype(np.float32)
+    beta = (1.0 / (1.0 + np.exp(-rng.standard_normal((B, n, H))))).astype(np.float32)
+    q, q32 = _to_dtype(q64, cfg.dtype)
+    k, k32 = _to_dtype(k64, cfg.dtype)
+    v, v32 = _to_dtype(v64, cfg.dtype)
+    return dict(q=q, k=k, v=v, q32=q32, k32=k32, v32=v32, alpha=alpha, beta=beta)
+
+
+def draw_state(cfg: Config, layer: int, batch: int | None = None) -> np.ndarray:
+    """Committed fp32 state H = S^T of one layer, [B][H][dk][dv]."""
+    B = cfg.batch if batch is None else batch
+    rng = _rng(base_seed(cfg), 2, layer)
+    s = rng.standard_normal((B, cfg.heads, cfg.d_k, cfg.d_v), dtype=np.float32)
+    s *= np.float32(0.02)
+    return s
+
+
+def draw_round(cfg: Config, round_index: int = 0, layers=None, batch: int | None = None) -> Round:
+    parent, path, length = draw_topology(cfg, round_index, batch)
+    r = Round(parent=parent, path=path, length=length)
+    for layer in (range(cfg.layers) if layers is None else layers):
+        d = draw_layer(cfg, layer, round_index, batch)
+        r.q.append(d["q"]); r.k.append(d["k"]); r.v.append(d["v"])
+        r.q32.append(d["q32"]); r.k32.append(d["k32"]); r.v32.append(d["v32"])
+        r.alpha.append(d["alpha"]); r.beta.append(d["beta"])
+    return r
