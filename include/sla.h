@@ -1,0 +1,203 @@
+/*
+ * sla.h -- C ABI of libsla: gated-delta-rule (GDN) speculative verification
+ * of draft chains and trees against a recurrent state, with a compact
+ * per-node factor store and accepted-path commit, for AMD MI355X (gfx950).
+ *
+ * Method: SpecLA, "Efficient Speculative Decoding for Linear-Attention
+ * Models" (arXiv 2607.16673).
+ *
+ * Notation.  One (batch b, head h) pair is a unit.  The committed state of a
+ * unit is S (d_v x d_k); it is stored transposed, H = S^T, row-major
+ * [d_k][d_v] with v fastest (the K x V_tile orientation of §4.1, "Tiling").
+ * A draft of n nodes is given as a parent array in topological order
+ * (§4.2): parent[j] = -1 makes node j a child of the committed state,
+ * otherwise parent[j] < j.  P(j) is the root path of node j, root first and
+ * j last.  The GDN step of node a is
+ *     S <- alpha_a S (I - beta_a k_a k_a^T) + beta_a v_a k_a^T
+ * and node j outputs o_j = S_j q_j, where S_j is the state after the steps
+ * of P(j) (j included) applied to the committed state.  Updates never flow
+ * between siblings (tree mask of §4.2).
+ *
+ * Conventions for every entry point.
+ *   - Pointers named as device memory must be device memory of the current
+ *     HIP device; all such buffers are owned by the caller.  The library
+ *     allocates nothing, keeps no state between calls, and is re-entrant.
+ *   - Work is enqueued on the given stream and runs asynchronously; the
+ *     call returns before the work finishes.
+ *   - A negative return value is an argument error detected on the host;
+ *     nothing was launched and no buffer was touched.
+ *   - Data errors that only the device can see (an invalid parent array or
+ *     accepted path in device memory) are reported per sequence in
+ *     status[b]; such a sequence's state is left untouched and its outputs
+ *     and factors are unspecified.  status may be NULL.
+ *   - All tensors are dense, contiguous and row-major in the stated shapes.
+ */
+#ifndef SLA_H_
+#define SLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+#define SLA_OK 0
+#define SLA_ERR_NULL (-1)        /* a required pointer is NULL             */
+#define SLA_ERR_SHAPE (-2)       /* a size is out of range                 */
+#define SLA_ERR_DTYPE (-3)       /* unknown activation dtype               */
+#define SLA_ERR_TOPOLOGY (-4)    /* parent array not in topological order  */
+#define SLA_ERR_PATH (-5)        /* accepted path is not a root path       */
+#define SLA_ERR_ALIAS (-6)       /* pending factors overlap output factors */
+#define SLA_ERR_UNSUPPORTED (-7) /* valid request this build cannot run    */
+#define SLA_ERR_HIP (-8)         /* the HIP runtime reported an error      */
+
+/* Activation dtypes of q, k, v (and of the stored k factor). */
+#define SLA_DTYPE_F32 0
+#define SLA_DTYPE_BF16 1
+
+/* Draft topology hint.  CHAIN promises parent[j] = j - 1 for every
+ * sequence (checked on the device; a violation is SLA_ERR_TOPOLOGY). */
+#define SLA_TOPO_TREE 0
+#define SLA_TOPO_CHAIN 1
+
+/* Verification route.
+ *   AUTO      the library chooses from the topology hint and the shape.
+ *   SERIAL    state-resident serial verification (§4.1): each node reduces
+ *             its parent state against k_j and q_j; chains advance the
+ *             on-chip state in place, trees rebuild a branch point's state
+ *             from the committed state and the stored factors.
+ *   PARALLEL  tree-masked factorised verification (§4.2): one dense
+ *             contraction of all queries and keys with the committed state
+ *             on the matrix cores, then a tree-masked triangular solve for
+ *             the corrected values and a tree-masked readout.            */
+#define SLA_ROUTE_AUTO 0
+#define SLA_ROUTE_SERIAL 1
+#define SLA_ROUTE_PARALLEL 2
+
+#define SLA_MAX_NODES 64
+
+typedef struct sla_shape {
+  int32_t batch;     /* B >= 1                                              */
+  int32_t heads;     /* H >= 1                                              */
+  int32_t d_k;       /* 64, 128 or 256                                      */
+  int32_t d_v;       /* multiple of 16, 16..1024                            */
+  int32_t n_nodes;   /* draft nodes per sequence, 1..SLA_MAX_NODES          */
+  int32_t qkv_dtype; /* SLA_DTYPE_F32 or SLA_DTYPE_BF16                     */
+  int32_t topology;  /* SLA_TOPO_TREE or SLA_TOPO_CHAIN                     */
+} sla_shape;
+
+/* Factor store (§5.1, factor buffering).  One record per node and head:
+ *   k     [B][n][H][d_k]  the node's key, in the activation dtype;
+ *   u     [B][n][H][d_v]  fp32 corrected value u_j = beta_j (v_j - alpha_j
+ *                         S_par k_j), with S_par the state of node j's parent;
+ *   alpha [B][n][H]       fp32 decay alpha_j;
+ *   parent[B][n]          int32 copy of the draft's parent array.
+ * With these, node j's state is S_j = alpha_j S_par + u_j k_j^T, so an
+ * accepted path is committed by rank-one updates alone (no reductions).
+ * All four are device memory written by sla_verify. */
+typedef struct sla_factors {
+  void *k;
+  float *u;
+  float *alpha;
+  int32_t *parent;
+} sla_factors;
+
+/* Pending accepted-factor buffer (§5.2, delayed state update): the factors
+ * of the previous verification and the path accepted from them.
+ *   f        factors written by the previous sla_verify (read only here);
+ *   n_nodes  that verification's n (its parent/path row length);
+ *   path     device [B][n_nodes] int32, node ids root first, -1 padded;
+ *   len      device [B] int32, accepted length 0..n_nodes.
+ * path[b][0..len[b]) must be a root path of f.parent[b]:
+ * parent[path[0]] = -1 and parent[path[t]] = path[t-1]. */
+typedef struct sla_pending {
+  sla_factors f;
+  int32_t n_nodes;
+  const int32_t *path;
+  const int32_t *len;
+} sla_pending;
+
+/* ------------------------------------------------------------ entry points */
+
+/* sla_verify -- verify one layer's drafts for all sequences (§4), storing
+ * the factor records (§5.1); optionally first commit a pending accepted
+ * path into the state (fused commit-and-verify, §5.2).
+ *
+ *   state   device fp32 [B][H][d_k][d_v].  With pending == NULL it is only
+ *           read.  Otherwise the pending path is applied and the committed
+ *           state is written back in place, and verification runs from the
+ *           committed state: one state read and one state write per call.
+ *   pending NULL, or the previous verification's factors and accepted path.
+ *           Its factor buffers must not overlap `factors` (ping-pong two
+ *           factor stores), else SLA_ERR_ALIAS.
+ *   q, k    device [B][n][H][d_k], shape->qkv_dtype.
+ *   v       device [B][n][H][d_v], shape->qkv_dtype.
+ *   alpha, beta  device fp32 [B][n][H]; decay and delta-rule strength.
+ *   parent_idx   device int32 [B][n]; topological order required.
+ *   out     device fp32 [B][n][H][d_v]; o_j = S_j q_j.
+ *   factors device factor store written for this draft (see sla_factors).
+ *   status  device int32 [B] or NULL: 0, SLA_ERR_TOPOLOGY or SLA_ERR_PATH.
+ *   route   SLA_ROUTE_*.
+ * Returns SLA_OK once the work is enqueued, or a negative error code. */
+int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pending *pending,
+               const void *q, const void *k, const void *v, const float *alpha,
+               const float *beta, const int32_t *parent_idx, float *out,
+               const sla_factors *factors, int32_t *status, hipStream_t stream);
+
+/* sla_commit -- immediate state update (§5.2): apply the accepted path's
+ * factor records to the state in place, S <- alpha_a S + u_a k_a^T for each
+ * accepted node a, root first.  shape->n_nodes is the n of the factors; path
+ * and len are as in sla_pending.  len[b] = 0 leaves sequence b untouched.
+ * The per-element arithmetic is the same as the pending prologue of
+ * sla_verify, so both routes give bitwise equal states.
+ *   state device fp32 [B][H][d_k][d_v]; factors: device (read only);
+ *   path device int32 [B][n]; len device int32 [B]; status device int32 [B]
+ *   or NULL (0 or SLA_ERR_PATH). */
+int sla_commit(const sla_shape *shape, float *state, const sla_factors *factors,
+               const int32_t *path, const int32_t *len, int32_t *status, hipStream_t stream);
+
+/* sla_topology -- the per-sequence topology table the verifier builds on
+ * chip (tree mask of §4.2), written out for inspection:
+ *   depth      int32 [B][n]   |P(j)|, a root has depth 1;
+ *   anc        uint64 [B][n]  bit a set iff node a is on P(j), j included;
+ *   order      int32 [B][n]   DFS pre-order: roots ascending, children
+ *                             ascending after their parent;
+ *   n_children int32 [B][n];
+ *   status     int32 [B]      0 or SLA_ERR_TOPOLOGY (then the row is
+ *                             unspecified).
+ * All pointers are device memory; none may be NULL. */
+int sla_topology(const int32_t *parent_idx, int32_t batch, int32_t n_nodes, int32_t *depth,
+                 uint64_t *anc, int32_t *order, int32_t *n_children, int32_t *status,
+                 hipStream_t stream);
+
+/* ------------------------------------------------------------ host helpers */
+
+/* Same table as sla_topology for one host-memory parent array, computed
+ * synchronously on the CPU; *max_depth may be NULL.  Returns SLA_OK,
+ * SLA_ERR_NULL, SLA_ERR_SHAPE or SLA_ERR_TOPOLOGY. */
+int sla_topology_host(const int32_t *parent_idx, int32_t n_nodes, int32_t *depth, uint64_t *anc,
+                      int32_t *order, int32_t *n_children, int32_t *max_depth);
+
+/* SLA_OK if path[0..len) (host memory) is a root path of the host parent
+ * array, else SLA_ERR_PATH (or SLA_ERR_TOPOLOGY for a bad parent array). */
+int sla_validate_path_host(const int32_t *parent_idx, int32_t n_nodes, const int32_t *path,
+                           int32_t len);
+
+/* Bytes of one factor store for this shape (k, u, alpha and parent). */
+size_t sla_factors_bytes(const sla_shape *shape);
+
+/* Static, human-readable name of a status code. */
+const char *sla_status_string(int status);
+
+/* Library ABI version (major * 10000 + minor * 100 + patch). */
+int sla_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SLA_H_ */

@@ -1,0 +1,258 @@
+"""Thin ctypes binding of libsla (C ABI in include/sla.h).
+
+Argument marshalling only: torch tensors are checked for device, dtype,
+shape and contiguity, turned into raw device pointers plus the current HIP
+stream, and passed to the library.  Every step of the verification and
+commit runs in the library's HIP kernels; there is no fallback of any kind.
+If ``libsla.so`` has not been built, every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsla.so")
+
+SLA_OK = 0
+SLA_ERR_NULL = -1
+SLA_ERR_SHAPE = -2
+SLA_ERR_DTYPE = -3
+SLA_ERR_TOPOLOGY = -4
+SLA_ERR_PATH = -5
+SLA_ERR_ALIAS = -6
+SLA_ERR_UNSUPPORTED = -7
+SLA_ERR_HIP = -8
+
+SLA_DTYPE_F32 = 0
+SLA_DTYPE_BF16 = 1
+SLA_TOPO_TREE = 0
+SLA_TOPO_CHAIN = 1
+SLA_ROUTE_AUTO = 0
+SLA_ROUTE_SERIAL = 1
+SLA_ROUTE_PARALLEL = 2
+SLA_MAX_NODES = 64
+
+ROUTES = {"auto": SLA_ROUTE_AUTO, "serial": SLA_ROUTE_SERIAL, "parallel": SLA_ROUTE_PARALLEL}
+TOPOLOGIES = {"tree": SLA_TOPO_TREE, "chain": SLA_TOPO_CHAIN}
+
+
+class SlaShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("d_k", ctypes.c_int32),
+                ("d_v", ctypes.c_int32), ("n_nodes", ctypes.c_int32), ("qkv_dtype", ctypes.c_int32),
+                ("topology", ctypes.c_int32)]
+
+
+class SlaFactors(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("u", ctypes.c_void_p), ("alpha", ctypes.c_void_p),
+                ("parent", ctypes.c_void_p)]
+
+
+class SlaPending(ctypes.Structure):
+    _fields_ = [("f", SlaFactors), ("n_nodes", ctypes.c_int32), ("path", ctypes.c_void_p),
+                ("len", ctypes.c_void_p)]
+
+
+class SlaError(RuntimeError):
+    def __init__(self, code: int, what: str = ""):
+        self.code = code
+        super().__init__("%s: %s (%d)" % (what or "libsla", status_string(code), code))
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libsla.so is not built (run `python -m paper_2607_16673_amd.build`)")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32 = ctypes.c_void_p, ctypes.c_int32
+        L.sla_verify.argtypes = [ctypes.POINTER(SlaShape), i32, vp, ctypes.POINTER(SlaPending),
+                                 vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(SlaFactors), vp, vp]
+        L.sla_verify.restype = ctypes.c_int
+        L.sla_commit.argtypes = [ctypes.POINTER(SlaShape), vp, ctypes.POINTER(SlaFactors), vp, vp, vp, vp]
+        L.sla_commit.restype = ctypes.c_int
+        L.sla_topology.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, vp]
+        L.sla_topology.restype = ctypes.c_int
+        L.sla_topology_host.argtypes = [vp, i32, vp, vp, vp, vp, vp]
+        L.sla_topology_host.restype = ctypes.c_int
+        L.sla_validate_path_host.argtypes = [vp, i32, vp, i32]
+        L.sla_validate_path_host.restype = ctypes.c_int
+        L.sla_factors_bytes.argtypes = [ctypes.POINTER(SlaShape)]
+        L.sla_factors_bytes.restype = ctypes.c_size_t
+        L.sla_status_string.argtypes = [ctypes.c_int]
+        L.sla_status_string.restype = ctypes.c_char_p
+        L.sla_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().sla_status_string(int(code)).decode()
+
+
+def sla_version() -> int:
+    return lib().sla_version()
+
+
+# ------------------------------------------------------------- host helpers
+def sla_topology_host(parent) -> dict:
+    p = np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    n = len(p)
+    depth = np.zeros(max(n, 1), np.int32)
+    anc = np.zeros(max(n, 1), np.uint64)
+    order = np.zeros(max(n, 1), np.int32)
+    kids = np.zeros(max(n, 1), np.int32)
+    md = np.zeros(1, np.int32)
+    st = lib().sla_topology_host(p.ctypes.data, n, depth.ctypes.data, anc.ctypes.data,
+                                 order.ctypes.data, kids.ctypes.data, md.ctypes.data)
+    return dict(status=st, depth=depth[:n], anc=anc[:n], order=order[:n], n_children=kids[:n],
+                max_depth=int(md[0]))
+
+
+def sla_validate_path_host(parent, path, length) -> int:
+    p = np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    pa = np.ascontiguousarray(np.asarray(path, dtype=np.int32)) if len(path) else np.zeros(1, np.int32)
+    return lib().sla_validate_path_host(p.ctypes.data, len(p), pa.ctypes.data, int(length))
+
+
+def make_shape(batch, heads, d_k, d_v, n_nodes, dtype="bf16", topology="tree") -> SlaShape:
+    return SlaShape(int(batch), int(heads), int(d_k), int(d_v), int(n_nodes),
+                    SLA_DTYPE_BF16 if dtype == "bf16" else SLA_DTYPE_F32, TOPOLOGIES[topology])
+
+
+def sla_factors_bytes(shape: SlaShape) -> int:
+    return int(lib().sla_factors_bytes(ctypes.byref(shape)))
+
+
+# ------------------------------------------------------------- device calls
+def _torch():
+    import torch
+    return torch
+
+
+def _dtype_code(t) -> int:
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return SLA_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return SLA_DTYPE_F32
+    raise TypeError("q/k/v must be bfloat16 or float32, got %s" % t.dtype)
+
+
+def _dev(t, dtype, shape, name):
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError("%s must be a torch tensor" % name)
+    if t.device.type != "cuda":
+        raise ValueError("%s must live on the GPU" % name)
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError("%s must be %s, got %s" % (name, dtype, t.dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    return ctypes.c_void_p(_torch().cuda.current_stream(device).cuda_stream)
+
+
+@dataclass
+class Factors:
+    """A factor store (see sla_factors in include/sla.h) as torch tensors."""
+    k: object       # [B][n][H][dk] activation dtype
+    u: object       # [B][n][H][dv] fp32
+    alpha: object   # [B][n][H] fp32
+    parent: object  # [B][n] int32
+
+    @staticmethod
+    def empty(batch, n, heads, d_k, d_v, dtype, device="cuda"):
+        torch = _torch()
+        return Factors(torch.empty(batch, n, heads, d_k, dtype=dtype, device=device),
+                       torch.empty(batch, n, heads, d_v, dtype=torch.float32, device=device),
+                       torch.empty(batch, n, heads, dtype=torch.float32, device=device),
+                       torch.empty(batch, n, dtype=torch.int32, device=device))
+
+    def c(self, dtype, B, n, H, dk, dv) -> SlaFactors:
+        torch = _torch()
+        return SlaFactors(_dev(self.k, dtype, (B, n, H, dk), "factors.k"),
+                          _dev(self.u, torch.float32, (B, n, H, dv), "factors.u"),
+                          _dev(self.alpha, torch.float32, (B, n, H), "factors.alpha"),
+                          _dev(self.parent, torch.int32, (B, n), "factors.parent"))
+
+
+def _check(code, what):
+    if code != SLA_OK:
+        raise SlaError(code, what)
+
+
+def sla_verify(state, q, k, v, alpha, beta, parent_idx, out, factors: Factors, *,
+               pending: Optional[tuple] = None, status=None, topology: str = "tree",
+               route: str = "auto"):
+    """Enqueue one verification on the current stream (see sla_verify in sla.h).
+
+    pending: None or (factors_prev: Factors, path [B][n_prev] int32, len [B] int32).
+    Raises SlaError on a host-detected error."""
+    torch = _torch()
+    B, n, H, dk = q.shape
+    dv = v.shape[-1]
+    dt = _dtype_code(q)
+    shape = SlaShape(B, H, dk, dv, n, dt, TOPOLOGIES[topology])
+    f = factors.c(q.dtype, B, n, H, dk, dv)
+    pend_p = None
+    if pending is not None:
+        pf, ppath, plen = pending
+        pn = pf.parent.shape[1]
+        pend = SlaPending(pf.c(q.dtype, B, pn, H, dk, dv), pn,
+                          _dev(ppath, torch.int32, (B, pn), "pending.path"),
+                          _dev(plen, torch.int32, (B,), "pending.len"))
+        pend_p = ctypes.byref(pend)
+    st_p = _dev(status, torch.int32, (B,), "status") if status is not None else None
+    code = lib().sla_verify(
+        ctypes.byref(shape), ROUTES[route], _dev(state, torch.float32, (B, H, dk, dv), "state"), pend_p,
+        _dev(q, q.dtype, (B, n, H, dk), "q"), _dev(k, q.dtype, (B, n, H, dk), "k"),
+        _dev(v, q.dtype, (B, n, H, dv), "v"), _dev(alpha, torch.float32, (B, n, H), "alpha"),
+        _dev(beta, torch.float32, (B, n, H), "beta"), _dev(parent_idx, torch.int32, (B, n), "parent_idx"),
+        _dev(out, torch.float32, (B, n, H, dv), "out"), ctypes.byref(f), st_p, _stream(q.device))
+    _check(code, "sla_verify")
+
+
+def sla_commit(state, factors: Factors, path, length, *, status=None):
+    """Enqueue an immediate commit of the accepted paths (see sla_commit)."""
+    torch = _torch()
+    B, n, H, dk = factors.k.shape
+    dv = factors.u.shape[-1]
+    shape = SlaShape(B, H, dk, dv, n, _dtype_code(factors.k), SLA_TOPO_TREE)
+    f = factors.c(factors.k.dtype, B, n, H, dk, dv)
+    st_p = _dev(status, torch.int32, (B,), "status") if status is not None else None
+    code = lib().sla_commit(ctypes.byref(shape), _dev(state, torch.float32, (B, H, dk, dv), "state"),
+                            ctypes.byref(f), _dev(path, torch.int32, (B, n), "path"),
+                            _dev(length, torch.int32, (B,), "len"), st_p, _stream(state.device))
+    _check(code, "sla_commit")
+
+
+def sla_topology(parent_idx):
+    """Device topology table (see sla_topology); returns tensors on the GPU."""
+    torch = _torch()
+    B, n = parent_idx.shape
+    dev = parent_idx.device
+    depth = torch.empty(B, n, dtype=torch.int32, device=dev)
+    anc = torch.empty(B, n, dtype=torch.int64, device=dev)
+    order = torch.empty(B, n, dtype=torch.int32, device=dev)
+    kids = torch.empty(B, n, dtype=torch.int32, device=dev)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    code = lib().sla_topology(_dev(parent_idx, torch.int32, (B, n), "parent_idx"), B, n,
+                              _dev(depth, None, None, "depth"), _dev(anc, None, None, "anc"),
+                              _dev(order, None, None, "order"), _dev(kids, None, None, "n_children"),
+                              _dev(status, None, None, "status"), _stream(dev))
+    _check(code, "sla_topology")
+    return dict(depth=depth, anc=anc, order=order, n_children=kids, status=status)

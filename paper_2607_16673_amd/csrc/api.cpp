@@ -1,0 +1,244 @@
+// api.cpp -- host side of the libsla C ABI (declared in include/sla.h):
+// argument validation, alias checks, route selection and kernel launches on
+// the caller's stream, plus the synchronous host topology helpers.
+// Nothing here allocates device memory or keeps state between calls.
+#include <stdint.h>
+#include <string.h>
+
+#include <vector>
+
+#include "kernels.hpp"
+#include "sla.h"
+
+namespace {
+
+constexpr int kVersion = 10000;  // 1.0.0
+
+bool dk_ok(int dk) { return dk == 64 || dk == 128 || dk == 256; }
+
+size_t act_bytes(int dtype) { return dtype == SLA_DTYPE_BF16 ? 2 : 4; }
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Range {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+Range range_of(const void *p, size_t bytes) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+  return Range{a, a + bytes};
+}
+
+bool overlaps(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
+
+int check_shape(const sla_shape *s) {
+  if (!s) return SLA_ERR_NULL;
+  if (s->batch < 1 || s->heads < 1 || s->n_nodes < 1 || s->n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+  if (s->d_k < 1 || s->d_v < 16 || s->d_v > 4096 || s->d_v % 16 != 0) return SLA_ERR_SHAPE;
+  if (s->qkv_dtype != SLA_DTYPE_F32 && s->qkv_dtype != SLA_DTYPE_BF16) return SLA_ERR_DTYPE;
+  if (s->topology != SLA_TOPO_TREE && s->topology != SLA_TOPO_CHAIN) return SLA_ERR_SHAPE;
+  if (!dk_ok(s->d_k)) return SLA_ERR_UNSUPPORTED;
+  // grid sizes stay far inside 2^31 workgroups
+  if ((uint64_t)s->batch * (uint64_t)s->heads * (uint64_t)(s->d_v / 16) > (1ull << 30)) return SLA_ERR_SHAPE;
+  return SLA_OK;
+}
+
+struct FactorSizes {
+  size_t k, u, alpha, parent;
+};
+
+FactorSizes factor_sizes(const sla_shape *s, int n) {
+  const size_t bnh = (size_t)s->batch * n * s->heads;
+  return FactorSizes{bnh * s->d_k * act_bytes(s->qkv_dtype), bnh * s->d_v * sizeof(float),
+                     bnh * sizeof(float), (size_t)s->batch * n * sizeof(int32_t)};
+}
+
+bool factors_complete(const sla_factors *f) { return f && f->k && f->u && f->alpha && f->parent; }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? SLA_OK : SLA_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int sla_version(void) { return kVersion; }
+
+const char *sla_status_string(int status) {
+  switch (status) {
+    case SLA_OK: return "ok";
+    case SLA_ERR_NULL: return "null pointer";
+    case SLA_ERR_SHAPE: return "size out of range";
+    case SLA_ERR_DTYPE: return "unknown activation dtype";
+    case SLA_ERR_TOPOLOGY: return "parent array is not in topological order";
+    case SLA_ERR_PATH: return "accepted path is not a root path";
+    case SLA_ERR_ALIAS: return "pending factors overlap output factors";
+    case SLA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case SLA_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+size_t sla_factors_bytes(const sla_shape *shape) {
+  if (check_shape(shape) != SLA_OK) return 0;
+  const FactorSizes f = factor_sizes(shape, shape->n_nodes);
+  return f.k + f.u + f.alpha + f.parent;
+}
+
+int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pending *pending,
+               const void *q, const void *k, const void *v, const float *alpha, const float *beta,
+               const int32_t *parent_idx, float *out, const sla_factors *factors, int32_t *status,
+               hipStream_t stream) {
+  int st = check_shape(shape);
+  if (st != SLA_OK) return st;
+  if (!state || !q || !k || !v || !alpha || !beta || !parent_idx || !out || !factors_complete(factors))
+    return SLA_ERR_NULL;
+  if (route != SLA_ROUTE_AUTO && route != SLA_ROUTE_SERIAL && route != SLA_ROUTE_PARALLEL) return SLA_ERR_SHAPE;
+  if (pending) {
+    if (!factors_complete(&pending->f) || !pending->path || !pending->len) return SLA_ERR_NULL;
+    if (pending->n_nodes < 1 || pending->n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+    const FactorSizes po = factor_sizes(shape, shape->n_nodes);
+    const FactorSizes pi = factor_sizes(shape, pending->n_nodes);
+    const Range outs[4] = {range_of(factors->k, po.k), range_of(factors->u, po.u),
+                           range_of(factors->alpha, po.alpha), range_of(factors->parent, po.parent)};
+    const Range ins[4] = {range_of(pending->f.k, pi.k), range_of(pending->f.u, pi.u),
+                          range_of(pending->f.alpha, pi.alpha), range_of(pending->f.parent, pi.parent)};
+    for (const Range &x : outs)
+      for (const Range &y : ins)
+        if (overlaps(x, y)) return SLA_ERR_ALIAS;
+    if (!aligned16(pending->f.k) || !aligned16(pending->f.u)) return SLA_ERR_UNSUPPORTED;
+  }
+  if (!aligned16(state) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
+      !aligned16(factors->k) || !aligned16(factors->u))
+    return SLA_ERR_UNSUPPORTED;
+
+  const bool chain = shape->topology == SLA_TOPO_CHAIN;
+  bool use_parallel;
+  if (route == SLA_ROUTE_PARALLEL) {
+    if (!sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes)) return SLA_ERR_UNSUPPORTED;
+    use_parallel = true;
+  } else if (route == SLA_ROUTE_SERIAL) {
+    use_parallel = false;
+  } else {
+    // Chains keep the state tile resident and advance it in place; branching
+    // drafts go to the tree-masked contraction when the shape allows it.
+    use_parallel = !chain && sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes);
+  }
+
+  sla::VerifyArgs a;
+  memset(&a, 0, sizeof(a));
+  a.B = shape->batch;
+  a.H = shape->heads;
+  a.dk = shape->d_k;
+  a.dv = shape->d_v;
+  a.n = shape->n_nodes;
+  a.chain = chain;
+  a.has_pending = pending != nullptr;
+  a.state = state;
+  if (pending) {
+    a.pend.k = pending->f.k;
+    a.pend.u = pending->f.u;
+    a.pend.alpha = pending->f.alpha;
+    a.pend.parent = pending->f.parent;
+    a.pend.n = pending->n_nodes;
+    a.pend.path = pending->path;
+    a.pend.len = pending->len;
+  }
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.alpha = alpha;
+  a.beta = beta;
+  a.parent = parent_idx;
+  a.out = out;
+  a.fk = factors->k;
+  a.fu = factors->u;
+  a.falpha = factors->alpha;
+  a.fparent = factors->parent;
+  a.status = status;
+  const hipError_t e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)
+                                    : sla::launch_verify_serial(a, shape->qkv_dtype, stream);
+  if (e == hipErrorInvalidConfiguration) return SLA_ERR_UNSUPPORTED;
+  return hip_status(e);
+}
+
+int sla_commit(const sla_shape *shape, float *state, const sla_factors *factors, const int32_t *path,
+               const int32_t *len, int32_t *status, hipStream_t stream) {
+  int st = check_shape(shape);
+  if (st != SLA_OK) return st;
+  if (!state || !factors_complete(factors) || !path || !len) return SLA_ERR_NULL;
+  if (!aligned16(state) || !aligned16(factors->u)) return SLA_ERR_UNSUPPORTED;
+  sla::CommitArgs a;
+  a.B = shape->batch;
+  a.H = shape->heads;
+  a.dk = shape->d_k;
+  a.dv = shape->d_v;
+  a.n = shape->n_nodes;
+  a.state = state;
+  a.k = factors->k;
+  a.u = factors->u;
+  a.alpha = factors->alpha;
+  a.parent = factors->parent;
+  a.path = path;
+  a.len = len;
+  a.status = status;
+  return hip_status(sla::launch_commit(a, shape->qkv_dtype, stream));
+}
+
+int sla_topology(const int32_t *parent_idx, int32_t batch, int32_t n_nodes, int32_t *depth, uint64_t *anc,
+                 int32_t *order, int32_t *n_children, int32_t *status, hipStream_t stream) {
+  if (!parent_idx || !depth || !anc || !order || !n_children || !status) return SLA_ERR_NULL;
+  if (batch < 1 || n_nodes < 1 || n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+  sla::TopologyArgs a{batch, n_nodes, parent_idx, depth, anc, order, n_children, status};
+  return hip_status(sla::launch_topology(a, stream));
+}
+
+// Host topology: depths and ancestor masks accumulate front to back (every
+// parent precedes its child), the pre-order comes from an explicit stack.
+int sla_topology_host(const int32_t *parent_idx, int32_t n, int32_t *depth, uint64_t *anc, int32_t *order,
+                      int32_t *n_children, int32_t *max_depth) {
+  if (!parent_idx || !depth || !anc || !order || !n_children) return SLA_ERR_NULL;
+  if (n < 1 || n > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+  for (int j = 0; j < n; ++j)
+    if (parent_idx[j] < -1 || parent_idx[j] >= j) return SLA_ERR_TOPOLOGY;
+  int md = 0;
+  for (int j = 0; j < n; ++j) {
+    const int p = parent_idx[j];
+    depth[j] = (p >= 0 ? depth[p] : 0) + 1;
+    anc[j] = (p >= 0 ? anc[p] : 0ull) | (1ull << j);
+    n_children[j] = 0;
+    if (depth[j] > md) md = depth[j];
+  }
+  for (int j = 0; j < n; ++j)
+    if (parent_idx[j] >= 0) ++n_children[parent_idx[j]];
+  std::vector<int> stack;
+  stack.reserve(n);
+  for (int j = n - 1; j >= 0; --j)
+    if (parent_idx[j] == -1) stack.push_back(j);
+  int pos = 0;
+  while (!stack.empty()) {
+    const int x = stack.back();
+    stack.pop_back();
+    order[pos++] = x;
+    for (int c = n - 1; c > x; --c)
+      if (parent_idx[c] == x) stack.push_back(c);
+  }
+  if (max_depth) *max_depth = md;
+  return SLA_OK;
+}
+
+int sla_validate_path_host(const int32_t *parent_idx, int32_t n, const int32_t *path, int32_t len) {
+  if (!parent_idx || (len > 0 && !path)) return SLA_ERR_NULL;
+  if (n < 1 || n > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+  for (int j = 0; j < n; ++j)
+    if (parent_idx[j] < -1 || parent_idx[j] >= j) return SLA_ERR_TOPOLOGY;
+  if (len < 0 || len > n) return SLA_ERR_PATH;
+  int prev = -1;
+  for (int t = 0; t < len; ++t) {
+    const int a = path[t];
+    if (a < 0 || a >= n || parent_idx[a] != prev) return SLA_ERR_PATH;
+    prev = a;
+  }
+  return SLA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,243 @@
+// verify_serial.hip -- state-resident serial verification (SpecLA §4.1),
+// with the delayed state update of §5.2 fused in front of it.
+//
+// One wavefront owns one (batch b, head h, 16-column V-tile) slice of the
+// transposed state H = S^T: the full d_k rows of 16 value columns (V-dimension
+// tiling keeps every output column local, §4.1 "Tiling").  Lane (g, c) holds
+// column c of the contiguous row block g*R .. g*R+R-1 (R = d_k / 4) in
+// registers, so a reduction over d_k is a per-lane dot product followed by
+// two cross-row-group shuffles.
+//
+// Per node j, with H_par the on-chip state of j's parent:
+//     a_j = H_par^T k_j,   b_j = H_par^T q_j,   u_j = beta_j (v_j - alpha_j a_j)
+//     o_j = alpha_j b_j + (k_j . q_j) u_j                     (= S_j q_j)
+//     H_j = alpha_j H_par + k_j u_j^T   (only if j has children)
+// which is the GDN step S_j = alpha_j S_par (I - beta_j k_j k_j^T) +
+// beta_j v_j k_j^T rewritten around the corrected value u_j (the factor
+// record stored for commit).  Nodes are visited in DFS pre-order; a chain
+// therefore advances the registers in place.  When the next node's parent is
+// not the state in registers (a branch point of a tree), that state is
+// rebuilt from the committed tile kept in registers by re-applying the
+// stored factors of the parent's root path -- rank-one updates only, the
+// reductions of shared prefixes are never repeated.
+#include "device.hpp"
+#include "kernels.hpp"
+
+namespace sla {
+namespace {
+
+constexpr int kCols = 16;
+constexpr int kGroups = kWave / kCols;
+
+template <int DK, typename T, bool CHAIN>
+__global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
+  constexpr int R = DK / kGroups;
+  const int lane = threadIdx.x;
+  const int c = lane & (kCols - 1);
+  const int g = lane / kCols;
+  const int H = a.H, dv = a.dv, n = a.n;
+  const int ntiles = dv / kCols;
+  int w = blockIdx.x;
+  const int tile = w % ntiles;
+  w /= ntiles;
+  const int h = w % H;
+  const int b = w / H;
+  const int col = tile * kCols + c;
+  const int row0 = g * R;
+  const size_t unit = (size_t)b * H + h;
+
+  // The state tile: the only state read of this call.
+  float *st = a.state + unit * DK * dv + col;
+  float H0[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) H0[r] = st[(size_t)(row0 + r) * dv];
+
+  // Topology table of this draft and validation of the pending path.
+  NodeTopo topo;
+  int err = build_topology(a.parent + (size_t)b * n, n, lane, CHAIN, topo);
+  int plen = 0;
+  if (err == SLA_OK && a.has_pending) {
+    plen = a.pend.len[b];
+    err = check_path(a.pend.parent + (size_t)b * a.pend.n, a.pend.n,
+                     a.pend.path + (size_t)b * a.pend.n, plen, lane);
+  }
+  if (tile == 0 && h == 0 && lane == 0 && a.status) a.status[b] = err;
+  if (err != SLA_OK) return;
+
+  // Stage this unit's draft in LDS.
+  extern __shared__ float lds[];
+  float *ks = lds;                   // [n][DK]
+  float *qs = ks + n * DK;           // [n][DK]
+  float *vs = qs + n * DK;           // [n][kCols]
+  float *us = vs + n * kCols;        // [n][kCols]
+  float *als = us + n * kCols;       // [n]
+  float *bes = als + n;              // [n]
+  int *ords = reinterpret_cast<int *>(bes + n);  // [n] DFS pre-order
+  int *pars = ords + n;              // [n]
+  int *kids = pars + n;              // [n]
+  uint64_t *ancs = reinterpret_cast<uint64_t *>(kids + n + (n & 1));  // [n]
+
+  const T *q = static_cast<const T *>(a.q);
+  const T *k = static_cast<const T *>(a.k);
+  const T *v = static_cast<const T *>(a.v);
+  for (int idx = lane; idx < n * DK; idx += kWave) {
+    const int j = idx / DK, i = idx % DK;
+    const size_t src = (((size_t)b * n + j) * H + h) * DK + i;
+    ks[idx] = to_f32(k[src]);
+    qs[idx] = to_f32(q[src]);
+  }
+  for (int idx = lane; idx < n * kCols; idx += kWave) {
+    const int j = idx / kCols, cc = idx % kCols;
+    vs[idx] = to_f32(v[(((size_t)b * n + j) * H + h) * dv + tile * kCols + cc]);
+  }
+  if (lane < n) {
+    const size_t s = ((size_t)b * n + lane) * H + h;
+    als[lane] = a.alpha[s];
+    bes[lane] = a.beta[s];
+    ords[topo.pos] = lane;
+    pars[lane] = topo.parent;
+    kids[lane] = topo.n_children;
+    ancs[lane] = topo.anc;
+  }
+  // Factor records that do not depend on the V-tile: written once per unit
+  // (k, alpha) and once per sequence (parent).
+  if (tile == 0) {
+    T *fk = static_cast<T *>(a.fk);
+    for (int idx = lane; idx < n * DK; idx += kWave) {
+      const int j = idx / DK, i = idx % DK;
+      const size_t s = (((size_t)b * n + j) * H + h) * DK + i;
+      fk[s] = k[s];
+    }
+    if (lane < n) {
+      a.falpha[((size_t)b * n + lane) * H + h] = a.alpha[((size_t)b * n + lane) * H + h];
+      if (h == 0) a.fparent[(size_t)b * n + lane] = topo.parent;
+    }
+  }
+  __syncthreads();
+
+  // Delayed state update: commit the previous round's accepted path into the
+  // tile, then write the committed tile back (the only state write).
+  if (a.has_pending) {
+    const T *pk = static_cast<const T *>(a.pend.k);
+    const int pn = a.pend.n;
+    for (int t = 0; t < plen; ++t) {
+      const int node = a.pend.path[(size_t)b * pn + t];
+      const size_t s = ((size_t)b * pn + node) * H + h;
+      const float al = a.pend.alpha[s];
+      const float u = a.pend.u[s * dv + col];
+      float kr[R];
+      load_f32<R>(pk + s * DK + row0, kr);
+#pragma unroll
+      for (int r = 0; r < R; ++r) H0[r] = apply_factor(H0[r], al, kr[r], u);
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) st[(size_t)(row0 + r) * dv] = H0[r];
+  }
+
+  // Node loop.
+  float Hc[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) Hc[r] = H0[r];
+  int cur = -1;  // node whose state Hc holds (-1: committed state)
+  for (int t = 0; t < n; ++t) {
+    const int j = CHAIN ? t : ords[t];
+    const int p = CHAIN ? t - 1 : pars[j];
+    if (!CHAIN && p != cur) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) Hc[r] = H0[r];
+      if (p >= 0) {
+        uint64_t m = ancs[p];
+        while (m) {
+          const int x = __builtin_ctzll(m);
+          m &= m - 1;
+          const float al = als[x];
+          const float u = us[x * kCols + c];
+          const float *kx = ks + x * DK + row0;
+#pragma unroll
+          for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], al, kx[r], u);
+        }
+      }
+    }
+    const float *kj = ks + j * DK + row0;
+    const float *qj = qs + j * DK + row0;
+    float sk = 0.f, sq = 0.f, kq = 0.f;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const float kr = kj[r], qr = qj[r];
+      sk = __builtin_fmaf(Hc[r], kr, sk);
+      sq = __builtin_fmaf(Hc[r], qr, sq);
+      kq = __builtin_fmaf(kr, qr, kq);
+    }
+    sk += __shfl_xor(sk, 16);
+    sq += __shfl_xor(sq, 16);
+    kq += __shfl_xor(kq, 16);
+    sk += __shfl_xor(sk, 32);
+    sq += __shfl_xor(sq, 32);
+    kq += __shfl_xor(kq, 32);
+    const float al = als[j], be = bes[j];
+    const float u = be * (vs[j * kCols + c] - al * sk);
+    const float o = __builtin_fmaf(kq, u, al * sq);
+    if (g == 0) {
+      const size_t s = ((size_t)b * n + j) * H + h;
+      a.out[s * dv + col] = o;
+      a.fu[s * dv + col] = u;
+      us[j * kCols + c] = u;
+    }
+    const bool internal = CHAIN ? (t + 1 < n) : (kids[j] > 0);
+    if (internal) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], al, kj[r], u);
+      cur = j;
+    } else {
+      cur = p;
+    }
+  }
+}
+
+size_t serial_lds_bytes(int n, int dk) {
+  return sizeof(float) * ((size_t)2 * n * dk + 2 * n * kCols + 2 * n) + sizeof(int) * (3 * n + (n & 1)) +
+         sizeof(uint64_t) * n;
+}
+
+// gfx950 gives one workgroup up to 160 KiB of LDS; above the default 64 KiB
+// the kernel has to opt in.
+constexpr size_t kMaxLds = 160 * 1024;
+constexpr size_t kDefaultLds = 64 * 1024;
+
+template <typename K>
+hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const VerifyArgs &a) {
+  if (lds > kMaxLds) return hipErrorInvalidConfiguration;
+  if (lds > kDefaultLds) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(kernel, grid, dim3(kWave), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int DK, typename T>
+hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
+  const dim3 grid((unsigned)((size_t)a.B * a.H * (a.dv / kCols)));
+  const size_t lds = serial_lds_bytes(a.n, DK);
+  if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true>, grid, lds, s, a);
+  return launch_with_lds(verify_serial_kernel<DK, T, false>, grid, lds, s, a);
+}
+
+template <typename T>
+hipError_t launch_t(const VerifyArgs &a, hipStream_t s) {
+  switch (a.dk) {
+    case 64: return launch_dk<64, T>(a, s);
+    case 128: return launch_dk<128, T>(a, s);
+    case 256: return launch_dk<256, T>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_verify_serial(const VerifyArgs &a, int dtype, hipStream_t s) {
+  return dtype == SLA_DTYPE_BF16 ? launch_t<bf16>(a, s) : launch_t<float>(a, s);
+}
+
+}  // namespace sla

@@ -1,0 +1,73 @@
+"""GPU parity at the full benchmark sizes, in the launch configuration the
+benchmark times: batched tree serving (B=64, 16 heads, dk=dv=128, 16-node
+trees, 24 layers) and the large-batch shapes (B=256, 16 heads, dk=128,
+dv=256; 64-node trees and the 1-node decode chain).  Two speculative rounds
+are run per layer -- the second with the first round's accepted paths
+pending (fused commit-and-verify) -- and sampled (b, h) units are checked
+against the oracle one by one; the whole committed-state tensor is checked
+against the standalone-commit route bitwise."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2607_16673_amd import binding as B
+from paper_2607_16673_amd import inputs
+
+from gpu_util import (TOL, Layer, new_factors, new_out, oracle_commit_units, oracle_verify_units,
+                      rel_err, sample_units, verify)
+
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+@pytest.mark.parametrize("name,layers_checked", [
+    ("batched_tree_serving", [0, 11, 23]),
+    ("large_batch_tree64", [0]),
+    ("large_batch_chain1", [0]),
+])
+def test_full_size_two_rounds(name, layers_checked):
+    cfg = inputs.config(name)
+    say("full-size %s: generating" % name)
+    r0 = inputs.draw_round(cfg, 0)
+    r1 = inputs.draw_round(cfg, 1)
+    units = sample_units(cfg, 24, 7)
+    worst_o = worst_s = 0.0
+    for layer in range(cfg.layers):
+        S0 = inputs.draw_state(cfg, layer)
+        L0, L1 = Layer(cfg, r0, layer), Layer(cfg, r1, layer)
+        f0, f1 = new_factors(cfg), new_factors(cfg)
+        out0, out1 = new_out(cfg), new_out(cfg)
+        state = torch.from_numpy(S0).cuda()
+        st = torch.full((cfg.batch,), 99, dtype=torch.int32, device="cuda")
+        say("full-size %s layer %d: fused rounds" % (name, layer))
+        verify(state, L0, out0, f0)
+        verify(state, L1, out1, f1, pending=(f0, L0.path, L0.length), status=st)
+        torch.cuda.synchronize()
+        assert (st.cpu().numpy() == 0).all()
+        if layer not in layers_checked:
+            continue
+        # standalone route on the same inputs must agree bitwise
+        sep = torch.from_numpy(S0).cuda()
+        g0 = new_factors(cfg)
+        verify(sep, L0, new_out(cfg), g0)
+        B.sla_commit(sep, g0, L0.path, L0.length)
+        torch.cuda.synchronize()
+        assert torch.equal(sep, state)
+        S1 = oracle_commit_units(S0, r0, layer, units)
+        gotS = state.cpu().numpy()
+        es = rel_err(np.stack([gotS[b, h] for b, h in units]), np.stack([S1[u] for u in units]))
+        S1full = S0.astype(np.float64)
+        for (b, h), s in S1.items():
+            S1full[b, h] = s
+        ref1 = oracle_verify_units(S1full, r1, layer, units)
+        ref0 = oracle_verify_units(S0, r0, layer, units)
+        g1, g0o = out1.cpu().numpy(), out0.cpu().numpy()
+        eo = max(rel_err(np.stack([g1[b, :, h] for b, h in units]), np.stack([ref1[u] for u in units])),
+                 rel_err(np.stack([g0o[b, :, h] for b, h in units]), np.stack([ref0[u] for u in units])))
+        say("full-size %s layer %d: state err %.3e output err %.3e" % (name, layer, es, eo))
+        worst_o, worst_s = max(worst_o, eo), max(worst_s, es)
+        del S1full
+    assert worst_o <= TOL[cfg.dtype] and worst_s <= TOL[cfg.dtype]
