@@ -1,0 +1,230 @@
+"""Benchmark: GDN-shaped speculative verify+commit on one MI355X.
+
+One step = one speculative round of the whole hot path for every layer of
+the workload: per layer one fused commit-and-verify call (the previous
+round's accepted paths are committed into the state tile, the state is
+written back once, the draft trees are verified from the committed tile and
+the factor store is written).  Inputs are seeded synthetic tensors that are
+already resident in HBM when the timed region starts.
+
+Prints one JSON line: verified tree-nodes/s (one node = one draft token
+through one layer, all heads), the achieved HBM bandwidth of the verify
+kernel from its algorithmic bytes and HIP-event durations, and the fp64
+oracle timed on the host cores on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E peak, GB/s
+
+DEFAULT_WORKLOAD = "batched_tree_serving"
+METRIC = "verified tree-nodes/sec + achieved HBM GB/s, GDN-shaped verify+commit"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(cfg, pending_len):
+    """Bytes one fused verify call must move for one layer: the state once in
+    and once out, the draft's q/k/v/alpha/beta/parent, the outputs, the
+    factor store, and the pending records of the accepted paths."""
+    B, H, dk, dv, n = cfg.batch, cfg.heads, cfg.d_k, cfg.d_v, cfg.n_nodes
+    w = 2 if cfg.dtype == "bf16" else 4
+    bnh = B * n * H
+    state = 2 * B * H * dk * dv * 4
+    draft = bnh * (2 * dk * w + dv * w + 8) + B * n * 4
+    out = bnh * dv * 4
+    factors = bnh * (dk * w + dv * 4 + 4) + B * n * 4
+    A = int(np.sum(pending_len))
+    pend = A * H * (dk * w + dv * 4 + 4) + A * 4 + B * 4 * 2 + B * n * 4
+    return state + draft + out + factors + pend
+
+
+def cpu_baseline(cfg, rounds, states, budget_s=12.0):
+    """The fp64 oracle (verify + commit by definition) on the host cores, on
+    whole layers of the same workload until about budget_s of CPU time."""
+    import oracle
+
+    r0 = rounds
+    t0 = time.perf_counter()
+    layers = 0
+    for layer in range(cfg.layers):
+        out, st = oracle.verify(states[layer], r0.q32[layer], r0.k32[layer], r0.v32[layer], r0.alpha[layer],
+                                r0.beta[layer], r0.parent)
+        S1, st2 = oracle.commit(states[layer], r0.k32[layer], r0.v32[layer], r0.alpha[layer],
+                                r0.beta[layer], r0.parent, r0.path, r0.length)
+        assert (st == 0).all() and (st2 == 0).all()
+        layers += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    nodes = layers * cfg.batch * cfg.n_nodes
+    return {"value": nodes / dt, "unit": "nodes/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d of %d layers of the %s workload (all %d sequences x %d heads), verify + commit "
+                      "of one round, %.1f s" % (layers, cfg.layers, cfg.name, cfg.batch, cfg.heads, dt)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--route", default="auto", choices=["auto", "serial", "parallel"])
+    ap.add_argument("--separate", action="store_true",
+                    help="time the separate route (verify, then standalone commit) instead of the fused one")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
+                    help="measured HBM bytes per launch from rocprofv3 counters (if present)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+              "(every (batch, head) unit is independent; sharding is described in DESIGN.md).",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2607_16673_amd import binding as B
+    from paper_2607_16673_amd import inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    B.lib()
+    cfg = inputs.config(args.workload)
+    topo = "chain" if cfg.chain else "tree"
+    log("bench: generating %s (%d layers)" % (cfg.name, cfg.layers))
+    rnd = inputs.draw_round(cfg, 0)
+    states_np = [inputs.draw_state(cfg, l) for l in range(cfg.layers)]
+
+    def act(x):
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    layers = []
+    for l in range(cfg.layers):
+        layers.append(dict(q=act(rnd.q[l]), k=act(rnd.k[l]), v=act(rnd.v[l]),
+                           alpha=torch.from_numpy(rnd.alpha[l]).to(dev),
+                           beta=torch.from_numpy(rnd.beta[l]).to(dev)))
+    parent = torch.from_numpy(rnd.parent).to(dev)
+    path = torch.from_numpy(rnd.path).to(dev)
+    length = torch.from_numpy(rnd.length).to(dev)
+    states = [torch.from_numpy(s).to(dev) for s in states_np]
+    fshape = (cfg.batch, cfg.n_nodes, cfg.heads, cfg.d_k, cfg.d_v)
+    fstores = [[B.Factors.empty(*fshape, adt, dev) for _ in range(cfg.layers)] for _ in range(2)]
+    outs = [torch.empty(cfg.batch, cfg.n_nodes, cfg.heads, cfg.d_v, dtype=torch.float32, device=dev)
+            for _ in range(cfg.layers)]
+    status = torch.zeros(cfg.batch, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    step_no = [0]
+
+    def step(events=None):
+        s = step_no[0]
+        cur, prev = fstores[s % 2], fstores[(s + 1) % 2]
+        for l in range(cfg.layers):
+            L = layers[l]
+            if events is not None:
+                events.append(torch.cuda.Event(enable_timing=True))
+                events[-1].record(stream)
+            if args.separate:
+                B.sla_verify(states[l], L["q"], L["k"], L["v"], L["alpha"], L["beta"], parent, outs[l], cur[l],
+                             status=status, topology=topo, route=args.route)
+                if events is not None:
+                    events.append(torch.cuda.Event(enable_timing=True))
+                    events[-1].record(stream)
+                B.sla_commit(states[l], cur[l], path, length, status=status)
+            else:
+                pend = (prev[l], path, length) if s > 0 else None
+                B.sla_verify(states[l], L["q"], L["k"], L["v"], L["alpha"], L["beta"], parent, outs[l], cur[l],
+                             pending=pend, status=status, topology=topo, route=args.route)
+            if events is not None:
+                events.append(torch.cuda.Event(enable_timing=True))
+                events[-1].record(stream)
+        step_no[0] += 1
+
+    log("bench: warmup %d" % args.warmup)
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    assert int(status.abs().max()) == 0, "device reported a data error"
+
+    log("bench: timing %d steps" % args.steps)
+    events = []
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(events)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    elapsed = t1 - t0
+    ms_per_step = 1e3 * elapsed / args.steps
+
+    # verify-kernel durations from the HIP events bracketing each launch
+    if args.separate:
+        per = 3
+        vdur = [events[i].elapsed_time(events[i + 1]) for i in range(0, len(events), per)]
+        cdur = [events[i + 1].elapsed_time(events[i + 2]) for i in range(0, len(events), per)]
+    else:
+        vdur = [events[i].elapsed_time(events[i + 1]) for i in range(0, len(events), 2)]
+        cdur = []
+    v_ms = float(np.mean(vdur))
+    bytes_launch = algorithmic_bytes(cfg, rnd.length)
+    if args.separate:
+        # without a pending path the verify reads the state only; commit reads and writes it
+        bytes_launch -= cfg.batch * cfg.heads * cfg.d_k * cfg.d_v * 4
+    achieved = bytes_launch / (v_ms * 1e-3) / 1e9
+    nodes = cfg.batch * cfg.n_nodes * cfg.layers * args.steps
+    value = nodes / elapsed
+    traffic = None
+    kernel = None
+    if os.path.exists(args.traffic_json):
+        with open(args.traffic_json) as f:
+            tj = json.load(f)
+        key = "%s/%s/%s" % (cfg.name, args.route, "separate" if args.separate else "fused")
+        if key in tj:
+            traffic = tj[key].get("bytes_per_launch")
+            kernel = tj[key].get("kernel")
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": kernel or "sla verify (%s route)" % args.route,
+            "algorithmic_bytes_per_launch": int(bytes_launch), "avg_launch_ms": round(v_ms, 5)}
+    line = {
+        "metric": METRIC, "value": round(value, 1), "unit": "nodes/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "heads": cfg.heads, "d_k": cfg.d_k,
+                   "d_v": cfg.d_v, "nodes_per_tree": cfg.n_nodes, "topology": topo,
+                   "max_depth": cfg.max_depth, "max_branch": cfg.max_branch, "layers": cfg.layers,
+                   "qkv_dtype": cfg.dtype, "state_dtype": "f32", "route": args.route,
+                   "commit": "separate" if args.separate else "fused", "parallelism": "single-gpu"},
+        "hbm_gbps": round(achieved, 1),
+        "roofline": roof,
+    }
+    if cdur:
+        line["commit_avg_launch_ms"] = round(float(np.mean(cdur)), 5)
+    if not args.no_cpu_baseline:
+        log("bench: oracle CPU baseline")
+        line["cpu_baseline"] = cpu_baseline(cfg, rnd, states_np)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -114,14 +114,14 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
   const bool chain = shape->topology == SLA_TOPO_CHAIN;
   bool use_parallel;
   if (route == SLA_ROUTE_PARALLEL) {
-    if (!sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes)) return SLA_ERR_UNSUPPORTED;
+    if (!sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype)) return SLA_ERR_UNSUPPORTED;
     use_parallel = true;
   } else if (route == SLA_ROUTE_SERIAL) {
     use_parallel = false;
   } else {
     // Chains keep the state tile resident and advance it in place; branching
     // drafts go to the tree-masked contraction when the shape allows it.
-    use_parallel = !chain && sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes);
+    use_parallel = !chain && sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype);
   }
 
   sla::VerifyArgs a;

@@ -60,7 +60,7 @@ struct TopologyArgs {
 // Each launcher returns hipSuccess or the launch error.  `dtype` is
 // SLA_DTYPE_F32 or SLA_DTYPE_BF16.
 hipError_t launch_verify_serial(const VerifyArgs &a, int dtype, hipStream_t s);
-bool parallel_supported(int dk, int dv, int n);
+bool parallel_supported(int dk, int dv, int n, int dtype);
 hipError_t launch_verify_parallel(const VerifyArgs &a, int dtype, hipStream_t s);
 hipError_t launch_commit(const CommitArgs &a, int dtype, hipStream_t s);
 hipError_t launch_topology(const TopologyArgs &a, hipStream_t s);

@@ -23,12 +23,14 @@ def say(*a):
     print(*a, flush=True)
 
 
-@pytest.mark.parametrize("name,layers_checked", [
-    ("batched_tree_serving", [0, 11, 23]),
-    ("large_batch_tree64", [0]),
-    ("large_batch_chain1", [0]),
+@pytest.mark.parametrize("name,layers_checked,route", [
+    ("batched_tree_serving", [0, 11, 23], "auto"),
+    ("batched_tree_serving", [5], "serial"),
+    ("large_batch_tree64", [0], "auto"),
+    ("large_batch_tree64", [0], "serial"),
+    ("large_batch_chain1", [0], "auto"),
 ])
-def test_full_size_two_rounds(name, layers_checked):
+def test_full_size_two_rounds(name, layers_checked, route):
     cfg = inputs.config(name)
     say("full-size %s: generating" % name)
     r0 = inputs.draw_round(cfg, 0)
@@ -42,9 +44,9 @@ def test_full_size_two_rounds(name, layers_checked):
         out0, out1 = new_out(cfg), new_out(cfg)
         state = torch.from_numpy(S0).cuda()
         st = torch.full((cfg.batch,), 99, dtype=torch.int32, device="cuda")
-        say("full-size %s layer %d: fused rounds" % (name, layer))
-        verify(state, L0, out0, f0)
-        verify(state, L1, out1, f1, pending=(f0, L0.path, L0.length), status=st)
+        say("full-size %s %s layer %d: fused rounds" % (name, route, layer))
+        verify(state, L0, out0, f0, route=route)
+        verify(state, L1, out1, f1, pending=(f0, L0.path, L0.length), status=st, route=route)
         torch.cuda.synchronize()
         assert (st.cpu().numpy() == 0).all()
         if layer not in layers_checked:
@@ -52,7 +54,7 @@ def test_full_size_two_rounds(name, layers_checked):
         # standalone route on the same inputs must agree bitwise
         sep = torch.from_numpy(S0).cuda()
         g0 = new_factors(cfg)
-        verify(sep, L0, new_out(cfg), g0)
+        verify(sep, L0, new_out(cfg), g0, route=route)
         B.sla_commit(sep, g0, L0.path, L0.length)
         torch.cuda.synchronize()
         assert torch.equal(sep, state)
@@ -67,7 +69,7 @@ def test_full_size_two_rounds(name, layers_checked):
         g1, g0o = out1.cpu().numpy(), out0.cpu().numpy()
         eo = max(rel_err(np.stack([g1[b, :, h] for b, h in units]), np.stack([ref1[u] for u in units])),
                  rel_err(np.stack([g0o[b, :, h] for b, h in units]), np.stack([ref0[u] for u in units])))
-        say("full-size %s layer %d: state err %.3e output err %.3e" % (name, layer, es, eo))
+        say("full-size %s %s layer %d: state err %.3e output err %.3e" % (name, route, layer, es, eo))
         worst_o, worst_s = max(worst_o, eo), max(worst_s, es)
         del S1full
     assert worst_o <= TOL[cfg.dtype] and worst_s <= TOL[cfg.dtype]
