@@ -2,28 +2,35 @@
 // with the delayed state update of §5.2 fused in front of it.
 //
 // Unrolling the gated delta rule along a root path gives, for every node j
-// (gamma_j = product of alpha over P(j), D_ja = gamma_j / gamma_a):
+// (gamma_j = product of alpha over P(j), D_ja = gamma_j / gamma_a, a in P(j)):
 //     H_j = gamma_j H0 + sum_{a in P(j)} D_ja k_a u_a^T
-//     u_j = beta_j (v_j - gamma_j H0^T k_j) - sum_{a in P(j), a != j} beta_j D_ja (k_j.k_a) u_a
-//     o_j = gamma_j H0^T q_j + sum_{a in P(j)} D_ja (q_j.k_a) u_a
-// i.e. the tree-masked UT form: the corrected values solve a unit lower-
-// triangular system whose off-diagonal entries are masked by strict
-// ancestry (the paper's T_tree = solve_tril(I - A_tree)), and the outputs
-// are a masked readout of them.  Only the committed state is ever read.
+//     (I + Lk) U = R,   R_j = beta_j (v_j - gamma_j H0^T k_j),
+//                       Lk_ja = beta_j D_ja (k_j . k_a)   for a in P(j), a != j
+//     O = Gamma Q H0 + Attn U,   Attn_ja = D_ja (q_j . k_a)   for a in P(j)
+// which is the tree-masked UT form: T = (I + Lk)^-1 is the paper's
+// T_tree = solve_tril(I - A_tree), and O = Q^ S0^T - Attn W S0^T + Attn U.
+// Here both per-column products are taken from R:
+//     U = T R,     O = Gamma P_q + M R,     M = Attn T,
+// so the only sequential work is the small per-unit T and M (each lane walks
+// its own node's root path), and everything that scales with the state's
+// columns runs on the matrix cores.  Only the committed state is read.
 //
-// Mapping (one workgroup = one (batch b, head h, 64-column V-tile), four
-// wavefronts of 16 columns each):
-//   * every lane loads 8 consecutive state rows of one column per 32-row
-//     K-step -- exactly the B-operand fragment of v_mfma_f32_16x16x32_bf16 --
-//     applies the pending accepted path, writes the committed tile back, and
-//     splits each fp32 value into bf16 hi + lo for the matrix cores;
-//   * P = [Q; K] H0 (2n x 64) and the tree-masked Grams [Q; K] K^T run on the
-//     matrix cores (q and k are exact in bf16, so the Grams are exact
-//     products with fp32 accumulation; H0 enters as hi + lo);
-//   * the triangular solve runs level by level over the tree in the MFMA
-//     accumulator layout, the corrected values go through LDS, and the
-//     masked readout follows.  Only ancestor pairs of the Gram are kept, in
-//     per-node compact lists.
+// One workgroup = one (batch b, head h, 64-column V-tile); four wavefronts of
+// 16 state columns each.
+//   setup   wave 0: topology, decays gamma, compact-list offsets;
+//           wave 1: validates the pending accepted path and stages its factor
+//                   records in LDS; waves 2-3: stage [Q; K] in LDS.
+//   state   each lane loads 8 consecutive rows of one column per 32-row
+//           K-step (the B fragment of v_mfma_f32_16x16x32_bf16), applies the
+//           pending path, writes the committed tile back, splits fp32 into
+//           bf16 hi + lo.
+//   P       [Q; K] H0 on the matrix cores (q, k exact in bf16).
+//   Gram    [Q; K] K^T tiles that hold ancestor pairs (exact products); the
+//           ancestor entries go to per-node compact lists (ordered by depth).
+//   T, M    per node, along its root path, in fp32 on the vector ALUs.
+//   U, O    T R and M R with v_mfma_f32_16x16x16bf16_1k, whose B fragment
+//           is exactly the accumulator layout that holds R; fp32 operands
+//           enter as bf16 hi + lo (three products).
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -31,25 +38,29 @@ namespace sla {
 namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / kWave;
 constexpr int kWaveCols = 16;
 constexpr int kTileCols = kWaves * kWaveCols;  // 64 state columns per workgroup
-constexpr int kUPitch = kTileCols + 4;         // fp32 row pitch of U in LDS
+constexpr int kPMax = 8;                       // pending steps staged in LDS
 
 template <int DK, int NP>
 struct Lds {
-  static constexpr int XP = DK + 8;                 // bf16 row pitch of [Q; K]
-  static constexpr int kX = 2 * NP * XP * 2;        // bytes of [Q; K]
-  static constexpr int kU = NP * kUPitch * 4;       // corrected values
-  static constexpr int kL = 2 * (NP * (NP + 1) / 2) * 4;  // compact masked Grams (worst case)
-  static constexpr int kTopo = NP * (8 + 4 * 6) + 16;
-  static constexpr int kBytes = kX + kU + kL + kTopo;
+  static constexpr int XP = DK + 8;                   // bf16 row pitch of [Q; K]
+  static constexpr int kList = NP * (NP + 1) / 2;     // compact list capacity (floats)
+  static constexpr int kXBytes = 2 * NP * XP * 2;
+  static constexpr int kListBytes = 4 * kList * 4;    // Lk, Lq, T, M
+  static constexpr int kA = kXBytes > kListBytes ? kXBytes : kListBytes;  // [Q; K], later the lists
+  static constexpr int kPk = kPMax * DK * 2;          // pending keys (bf16)
+  static constexpr int kPu = kPMax * kTileCols * 4;   // pending corrected values of this tile
+  static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 8 + 16;
+  static constexpr int kBytes = kA + kPk + kPu + kTopo;
 };
 
-__device__ __forceinline__ bf16x8 pack_hi_lo(const float (&x)[8], bf16x8 &lo) {
+__device__ __forceinline__ bf16x8 split8(const float (&x)[8], bf16x8 &lo) {
   bf16x8 hi;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -60,33 +71,52 @@ __device__ __forceinline__ bf16x8 pack_hi_lo(const float (&x)[8], bf16x8 &lo) {
   return hi;
 }
 
+__device__ __forceinline__ void split4(const float (&x)[4], s16x4 &hi, s16x4 &lo) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const __bf16 h = static_cast<__bf16>(x[e]);
+    hi[e] = __builtin_bit_cast(short, h);
+    lo[e] = __builtin_bit_cast(short, static_cast<__bf16>(x[e] - static_cast<float>(h)));
+  }
+}
+
+__device__ __forceinline__ f32x4 mfma16(s16x4 a, s16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
 template <int DK, int NP>
 __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a) {
-  constexpr int KS = DK / 32;   // K-steps of the contraction over d_k
-  constexpr int NT = NP / 16;   // 16-node tiles
-  constexpr int MT = 2 * NT;    // 16-row tiles of [Q; K]
+  constexpr int KS = DK / 32;  // K-steps of the contraction over d_k
+  constexpr int NT = NP / 16;  // 16-node tiles
+  constexpr int MT = 2 * NT;   // 16-row tiles of [Q; K]
+  constexpr int CH = DK / 8;   // 16-byte chunks per [Q; K] row
+  constexpr int GT = (NT * (NT + 1) + kWaves - 1) / kWaves;  // Gram tiles per wave
   using L = Lds<DK, NP>;
 
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  __bf16 *xs = reinterpret_cast<__bf16 *>(lds);                          // [2NP][XP]
-  float *us = reinterpret_cast<float *>(lds + L::kX);                    // [NP][kUPitch]
-  float *lq = reinterpret_cast<float *>(lds + L::kX + L::kU);            // compact, by node
-  float *lk = lq + NP * (NP + 1) / 2;
-  unsigned char *tp = lds + L::kX + L::kU + L::kL;
-  uint64_t *s_anc = reinterpret_cast<uint64_t *>(tp);                    // [NP]
-  int *s_par = reinterpret_cast<int *>(tp + 8 * NP);                     // [NP]
-  int *s_depth = s_par + NP;                                             // [NP]
-  int *s_off = s_depth + NP;                                             // [NP]
-  float *s_gamma = reinterpret_cast<float *>(s_off + NP);                // [NP]
-  float *s_al = s_gamma + NP;                                            // [NP]
-  float *s_be = s_al + NP;                                               // [NP]
-  int *s_misc = reinterpret_cast<int *>(s_be + NP);                      // err, max depth
+  __bf16 *xs = reinterpret_cast<__bf16 *>(lds);            // [2NP][XP], phase 1
+  float *lk = reinterpret_cast<float *>(lds);              // compact lists, phase 2
+  float *lq = lk + L::kList;
+  float *tl = lq + L::kList;
+  float *ml = tl + L::kList;
+  __bf16 *s_pk = reinterpret_cast<__bf16 *>(lds + L::kA);  // [kPMax][DK]
+  float *s_pu = reinterpret_cast<float *>(lds + L::kA + L::kPk);  // [kPMax][64]
+  unsigned char *tp = lds + L::kA + L::kPk + L::kPu;
+  uint64_t *s_anc = reinterpret_cast<uint64_t *>(tp);      // [NP]
+  int *s_depth = reinterpret_cast<int *>(tp + 8 * NP);     // [NP]
+  int *s_off = s_depth + NP;                                // [NP]
+  float *s_gamma = reinterpret_cast<float *>(s_off + NP);  // [NP]
+  float *s_rgamma = s_gamma + NP;                           // [NP] 1 / gamma
+  float *s_be = s_rgamma + NP;                              // [NP]
+  int *s_pnode = reinterpret_cast<int *>(s_be + NP);        // [kPMax]
+  float *s_palpha = reinterpret_cast<float *>(s_pnode + kPMax);  // [kPMax]
+  int *s_misc = reinterpret_cast<int *>(s_palpha + kPMax);  // topo err, max depth, path err, path len
 
   const int tid = threadIdx.x;
   const int w = tid / kWave;
   const int l = tid % kWave;
-  const int lc = l & 15;   // column within the wave's 16, row within a 16-row tile
-  const int lg = l >> 4;   // 8-row group within a K-step / 4-row group of a C tile
+  const int lc = l & 15;  // column within the wave's 16 / row within a 16-row tile
+  const int lg = l >> 4;  // row group
   const int H = a.H, dv = a.dv, n = a.n;
   const int ntiles = (dv + kTileCols - 1) / kTileCols;
   int wid = blockIdx.x;
@@ -94,113 +124,163 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
   wid /= ntiles;
   const int h = wid % H;
   const int b = wid / H;
-  const int cw = tile * kTileCols + w * kWaveCols;  // first column of this wave
-  const bool cols_live = cw < dv;
-  const int col = cw + lc;
+  const int ucol = w * kWaveCols + lc;  // column within the tile
+  const int col = tile * kTileCols + ucol;
+  const bool cols_live = tile * kTileCols + w * kWaveCols < dv;  // wave-uniform
   const size_t unit = (size_t)b * H + h;
+  const size_t nbase = (size_t)b * n;
+  const bf16 *qg = static_cast<const bf16 *>(a.q);
+  const bf16 *kg = static_cast<const bf16 *>(a.k);
+  const bf16 *vg = static_cast<const bf16 *>(a.v);
 
-  // 1. The state tile straight into B-operand order (the only state read).
+  // ---- independent loads first: the state tile (the only state read) and
+  //      the values of the nodes whose accumulator rows this lane holds.
   float *st = a.state + unit * DK * dv + col;
   float hf[KS][8];
+  float vreg[NT][4];
   if (cols_live) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int e = 0; e < 8; ++e) hf[ks][e] = st[(size_t)(ks * 32 + 8 * lg + e) * dv];
-  }
-
-  // 2. Topology, decays and compact-list offsets (wave 0).
-  if (w == 0) {
-    NodeTopo t;
-    int err = build_topology(a.parent + (size_t)b * n, n, l, a.chain, t);
-    if (err == SLA_OK && a.has_pending)
-      err = check_path(a.pend.parent + (size_t)b * a.pend.n, a.pend.n, a.pend.path + (size_t)b * a.pend.n,
-                       a.pend.len[b], l);
-    if (err == SLA_OK) {
-      const bool live = l < n;
-      const size_t s = ((size_t)b * n + (live ? l : 0)) * H + h;
-      const float al = live ? a.alpha[s] : 1.f;
-      const float be = live ? a.beta[s] : 0.f;
-      float g = 1.f;
-      int off = 0, md = 0;
-      for (int i = 0; i < n; ++i) {
-        const float ai = __shfl(al, i);
-        if ((t.anc >> i) & 1ull) g *= ai;  // root first
-        const int di = __builtin_amdgcn_readlane(t.depth, i);
-        if (i < l) off += di;
-        md = di > md ? di : md;
-      }
-      if (live) {
-        s_anc[l] = t.anc;
-        s_par[l] = t.parent;
-        s_depth[l] = t.depth;
-        s_off[l] = off;
-        s_gamma[l] = g;
-        s_al[l] = al;
-        s_be[l] = be;
-      }
-      if (l == 0) s_misc[1] = md;
-    }
-    if (l == 0) s_misc[0] = err;
-  }
-  __syncthreads();
-  const int err = s_misc[0];
-  if (tile == 0 && h == 0 && tid == 0 && a.status) a.status[b] = err;
-  if (err != SLA_OK) return;
-  const int maxd = s_misc[1];
-
-  // 3. Stage [Q; K] (rows 0..NP-1: q_j, rows NP..2NP-1: k_j; zero padding).
-  {
-    const bf16 *q = static_cast<const bf16 *>(a.q);
-    const bf16 *k = static_cast<const bf16 *>(a.k);
-    constexpr int CH = DK / 8;  // 16-byte chunks per row
-    for (int c = tid; c < 2 * NP * CH; c += kThreads) {
-      const int row = c / CH, part = c % CH;
-      const int j = row % NP;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (j < n) {
-        const bf16 *src = (row < NP ? q : k) + (((size_t)b * n + j) * H + h) * DK + part * 8;
-        val = *reinterpret_cast<const uint4 *>(src);
-      }
-      *reinterpret_cast<uint4 *>(xs + row * L::XP + part * 8) = val;
-    }
-    if (tile == 0) {
-      // factor records independent of the V-tile
-      bf16 *fk = static_cast<bf16 *>(a.fk);
-      for (int c = tid; c < n * CH; c += kThreads) {
-        const int j = c / CH, part = c % CH;
-        const size_t off = (((size_t)b * n + j) * H + h) * DK + part * 8;
-        *reinterpret_cast<uint4 *>(fk + off) = *reinterpret_cast<const uint4 *>(k + off);
-      }
-      if (tid < n) {
-        const size_t s = ((size_t)b * n + tid) * H + h;
-        a.falpha[s] = a.alpha[s];
-        if (h == 0) a.fparent[(size_t)b * n + tid] = a.parent[(size_t)b * n + tid];
-      }
-    }
-  }
-
-  // values of the nodes this lane solves for (accumulator rows 4*lg + r)
-  float vreg[NT][4];
-  if (cols_live) {
-    const bf16 *v = static_cast<const bf16 *>(a.v);
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int j = mt * 16 + 4 * lg + r;
-        vreg[mt][r] = j < n ? to_f32(v[(((size_t)b * n + j) * H + h) * dv + col]) : 0.f;
+        vreg[mt][r] = j < n ? to_f32(vg[((nbase + j) * H + h) * dv + col]) : 0.f;
       }
   }
 
-  // 4. Delayed state update on the registers, write-back, hi/lo split.
+  // ---- setup, one job per wavefront
+  if (w == 0) {
+    // topology, decays and compact-list offsets; lane j owns node j
+    const bool live = l < n;
+    const int p = live ? a.parent[nbase + l] : -1;
+    bool bad = live && (p < -1 || p >= l);
+    if (a.chain) bad = bad || (live && p != l - 1);
+    const int err = wave_any(bad) ? SLA_ERR_TOPOLOGY : SLA_OK;
+    if (err == SLA_OK) {
+      const size_t s = ((nbase + (live ? l : 0)) * H + h);
+      const float al = live ? a.alpha[s] : 1.f;
+      const float be = live ? a.beta[s] : 0.f;
+      uint64_t m = live ? (1ull << l) : 0ull;
+      float g = al;
+      int d = live ? 1 : 0;
+      int x = p;
+      while (wave_any(x >= 0)) {
+        const int src = x >= 0 ? x : 0;
+        const float ax = __shfl(al, src);
+        const int px = __shfl(p, src);
+        if (x >= 0) {
+          m |= 1ull << x;
+          g *= ax;
+          ++d;
+        }
+        x = x >= 0 ? px : -1;
+      }
+      int incl = d;  // inclusive prefix sum of depths -> list offsets
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (l >= o) incl += y;
+      }
+      int md = d;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) md = max(md, __shfl_xor(md, o));
+      if (live) {
+        s_anc[l] = m;
+        s_depth[l] = d;
+        s_off[l] = incl - d;
+        s_gamma[l] = g;
+        s_rgamma[l] = 1.f / g;
+        s_be[l] = be;
+      }
+      if (l == 0) s_misc[1] = md;
+    }
+    if (l == 0) s_misc[0] = err;
+  } else if (w == 1) {
+    // pending accepted path: validate, then stage its records in LDS
+    int perr = SLA_OK, plen = 0;
+    if (a.has_pending) {
+      const int pn = a.pend.n;
+      plen = a.pend.len[b];
+      perr = check_path(a.pend.parent + (size_t)b * pn, pn, a.pend.path + (size_t)b * pn, plen, l);
+      if (perr == SLA_OK) {
+        const int ps = plen < kPMax ? plen : kPMax;
+        if (l < ps) {
+          const int node = a.pend.path[(size_t)b * pn + l];
+          s_pnode[l] = node;
+          s_palpha[l] = a.pend.alpha[((size_t)b * pn + node) * H + h];
+        }
+        __builtin_amdgcn_wave_barrier();
+        const bf16 *pk = static_cast<const bf16 *>(a.pend.k);
+        for (int c = l; c < ps * CH; c += kWave) {
+          const int t = c / CH, part = c % CH;
+          const size_t src = (((size_t)b * pn + s_pnode[t]) * H + h) * DK + part * 8;
+          *reinterpret_cast<uint4 *>(s_pk + t * DK + part * 8) = *reinterpret_cast<const uint4 *>(pk + src);
+        }
+        for (int t = 0; t < ps; ++t) {
+          const int cg = tile * kTileCols + l;
+          s_pu[t * kTileCols + l] =
+              cg < dv ? a.pend.u[(((size_t)b * pn + s_pnode[t]) * H + h) * dv + cg] : 0.f;
+        }
+      }
+    }
+    if (l == 0) {
+      s_misc[2] = perr;
+      s_misc[3] = plen;
+    }
+  } else {
+    // [Q; K]: rows 0..NP-1 hold q_j, rows NP..2NP-1 hold k_j; zero padding
+    for (int c = tid - 2 * kWave; c < 2 * NP * CH; c += 2 * kWave) {
+      const int row = c / CH, part = c % CH;
+      const int j = row % NP;
+      uint4 val = make_uint4(0, 0, 0, 0);
+      if (j < n) val = *reinterpret_cast<const uint4 *>((row < NP ? qg : kg) + ((nbase + j) * H + h) * DK + part * 8);
+      *reinterpret_cast<uint4 *>(xs + row * L::XP + part * 8) = val;
+    }
+  }
+  __syncthreads();
+  const int err = s_misc[0] != SLA_OK ? s_misc[0] : s_misc[2];
+  if (tile == 0 && h == 0 && tid == 0 && a.status) a.status[b] = err;
+  if (err != SLA_OK) return;
+  const int plen = s_misc[3];
+
+  // ---- factor records that do not depend on the V-tile
+  if (tile == 0) {
+    bf16 *fk = static_cast<bf16 *>(a.fk);
+    for (int c = tid; c < n * CH; c += kThreads) {
+      const int j = c / CH, part = c % CH;
+      *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * 8) =
+          *reinterpret_cast<const uint4 *>(xs + (NP + j) * L::XP + part * 8);
+    }
+    if (tid < n) {
+      const size_t s = (nbase + tid) * H + h;
+      a.falpha[s] = a.alpha[s];
+      if (h == 0) a.fparent[nbase + tid] = a.parent[nbase + tid];
+    }
+  }
+
+  // ---- delayed state update on the registers, write-back, hi/lo split
   bf16x8 bhi[KS], blo[KS];
   if (cols_live) {
     if (a.has_pending) {
+      const int ps = plen < kPMax ? plen : kPMax;
+      for (int t = 0; t < ps; ++t) {
+        const float al = s_palpha[t];
+        const float u = s_pu[t * kTileCols + ucol];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(s_pk + t * DK + ks * 32 + 8 * lg);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, static_cast<float>(kv[e]), u);
+        }
+      }
+      // paths longer than the LDS stage read their records directly
       const bf16 *pk = static_cast<const bf16 *>(a.pend.k);
       const int pn = a.pend.n;
-      const int plen = a.pend.len[b];
-      for (int t = 0; t < plen; ++t) {
+      for (int t = kPMax; t < plen; ++t) {
         const int node = a.pend.path[(size_t)b * pn + t];
         const size_t s = ((size_t)b * pn + node) * H + h;
         const float al = a.pend.alpha[s];
@@ -219,18 +299,18 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
         for (int e = 0; e < 8; ++e) st[(size_t)(ks * 32 + 8 * lg + e) * dv] = hf[ks][e];
     }
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) bhi[ks] = pack_hi_lo(hf[ks], blo[ks]);
+    for (int ks = 0; ks < KS; ++ks) bhi[ks] = split8(hf[ks], blo[ks]);
   }
-  __syncthreads();  // [Q; K] staged
 
-  // 5. Matrix cores: P = [Q; K] H0 for this wave's 16 columns.
+  // ---- P = [Q; K] H0 for this wave's 16 columns (accumulator layout: lane
+  //      (lg, lc) holds rows 4 lg .. 4 lg + 3 of each 16-row tile, column lc)
   f32x4 pacc[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) pacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
   if (cols_live) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      if ((mt % NT) * 16 >= n) continue;  // rows of padding only
+      if ((mt % NT) * 16 >= n) continue;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + (mt * 16 + lc) * L::XP + ks * 32 + 8 * lg);
@@ -240,93 +320,161 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
     }
   }
 
-  // 6. Tree-masked Grams: tiles (row tile mr of [Q; K], node tile na) that
-  //    contain an ancestor pair, spread over the waves; each lane scatters
-  //    its ancestor entries into the per-node compact lists.
+  // ---- tree-masked Grams: tile (mr, na) of [Q; K] K^T holds rows of node
+  //      tile jt = mr % NT against ancestor candidates of node tile na <= jt
+  f32x4 gacc[GT];
+#pragma unroll
+  for (int i = 0; i < GT; ++i) gacc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
   {
-    int tcount = 0;
-    for (int mr = 0; mr < MT; ++mr) {
-      const int jt = mr % NT;
-      if (jt * 16 >= n) continue;
-      for (int na = 0; na <= jt; ++na, ++tcount) {
-        if (tcount % kWaves != w) continue;
-        f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f};
+    int tc = 0;
+#pragma unroll
+    for (int mr = 0; mr < MT; ++mr)
+#pragma unroll
+      for (int na = 0; na <= mr % NT; ++na, ++tc) {
+        if (tc % kWaves != w || (mr % NT) * 16 >= n) continue;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + (mr * 16 + lc) * L::XP + ks * 32 + 8 * lg);
           const bf16x8 bf =
               *reinterpret_cast<const bf16x8 *>(xs + (NP + na * 16 + lc) * L::XP + ks * 32 + 8 * lg);
-          g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, g, 0, 0, 0);
+          gacc[tc / kWaves] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, gacc[tc / kWaves], 0, 0, 0);
         }
-        const int an = na * 16 + lc;  // ancestor candidate (column of the tile)
+      }
+  }
+  __syncthreads();  // [Q; K] is dead from here on; its space holds the lists
+
+  // ---- scatter ancestor entries of the Grams into the compact lists:
+  //      entry (j, a) of a list lives at off_j + depth(a) - 1
+  {
+    int tc = 0;
+#pragma unroll
+    for (int mr = 0; mr < MT; ++mr)
+#pragma unroll
+      for (int na = 0; na <= mr % NT; ++na, ++tc) {
+        if (tc % kWaves != w || (mr % NT) * 16 >= n) continue;
+        const int an = na * 16 + lc;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int j = jt * 16 + 4 * lg + r;
+          const int j = (mr % NT) * 16 + 4 * lg + r;
           if (j >= n || an > j) continue;
           const uint64_t m = s_anc[j];
           if (!((m >> an) & 1ull)) continue;
-          const int rank = __popcll(m & ((1ull << an) - 1ull));
-          const float dja = s_gamma[j] / s_gamma[an];
-          if (mr < NT) {
-            lq[s_off[j] + rank] = dja * g[r];
-          } else if (an < j) {
-            lk[s_off[j] + rank] = s_be[j] * dja * g[r];
-          }
+          const int idx = s_off[j] + s_depth[an] - 1;
+          const float dja = s_gamma[j] * s_rgamma[an];
+          const float gv = gacc[tc / kWaves][r];
+          if (mr < NT)
+            lq[idx] = dja * gv;
+          else if (an < j)
+            lk[idx] = s_be[j] * dja * gv;
         }
       }
-    }
-  }
-  __syncthreads();  // compact lists complete
-
-  // 7. Level-synchronous solve for the corrected values u (accumulator rows
-  //    of the K half), written to LDS and to the factor store.
-  const size_t obase = (size_t)b * n;
-  const int ucol = w * kWaveCols + lc;
-  for (int d = 1; d <= maxd; ++d) {
-    if (cols_live) {
-#pragma unroll
-      for (int mt = 0; mt < NT; ++mt)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int j = mt * 16 + 4 * lg + r;
-          if (j >= n || s_depth[j] != d) continue;
-          const float gj = s_gamma[j], bj = s_be[j];
-          float s = bj * (vreg[mt][r] - gj * pacc[NT + mt][r]);
-          uint64_t m = s_anc[j] & ~(1ull << j);
-          const float *lkj = lk + s_off[j];
-          int idx = 0;
-          while (m) {
-            const int an = __builtin_ctzll(m);
-            m &= m - 1ull;
-            s -= lkj[idx++] * us[an * kUPitch + ucol];
-          }
-          us[j * kUPitch + ucol] = s;
-          a.fu[((obase + j) * H + h) * dv + col] = s;
-        }
-    }
-    __syncthreads();
   }
 
-  // 8. Masked readout o_j = gamma_j q_j^T H0 + sum_{a in P(j)} D_ja (q_j.k_a) u_a.
-  if (cols_live) {
+  // ---- R = beta (v - gamma P_k) in the accumulator layout
+  float rreg[NT][4];
 #pragma unroll
-    for (int mt = 0; mt < NT; ++mt)
+  for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int j = mt * 16 + 4 * lg + r;
-        if (j >= n) continue;
-        float o = s_gamma[j] * pacc[mt][r];
-        uint64_t m = s_anc[j];
-        const float *lqj = lq + s_off[j];
-        int idx = 0;
-        while (m) {
-          const int an = __builtin_ctzll(m);
-          m &= m - 1ull;
-          o = __builtin_fmaf(lqj[idx++], us[an * kUPitch + ucol], o);
-        }
-        a.out[((obase + j) * H + h) * dv + col] = o;
+    for (int r = 0; r < 4; ++r) {
+      const int j = mt * 16 + 4 * lg + r;
+      rreg[mt][r] = (cols_live && j < n) ? s_be[j] * (vreg[mt][r] - s_gamma[j] * pacc[NT + mt][r]) : 0.f;
+    }
+  __syncthreads();  // lists complete
+
+  // ---- T = (I + Lk)^-1, row j along P(j) (deepest ancestor first):
+  //      T_jj = 1,  T_ja = - sum_{e in P(j), a < e} T_je Lk_ea
+  if (tid < n) {
+    const int j = tid;
+    const uint64_t m = s_anc[j];
+    const int off = s_off[j];
+    tl[off + s_depth[j] - 1] = 1.f;
+    uint64_t rest = m & ~(1ull << j);
+    while (rest) {
+      const int an = 63 - __builtin_clzll(rest);
+      rest &= ~(1ull << an);
+      const int ta = s_depth[an] - 1;
+      uint64_t below = m & ~((2ull << an) - 1ull);
+      float s = 0.f;
+      while (below) {
+        const int e = __builtin_ctzll(below);
+        below &= below - 1ull;
+        s = __builtin_fmaf(-tl[off + s_depth[e] - 1], lk[s_off[e] + ta], s);
       }
+      tl[off + ta] = s;
+    }
   }
+  __syncthreads();
+
+  // ---- M = Attn T, row j:  M_ja = sum_{e in P(j), a <= e} Attn_je T_ea
+  if (tid < n) {
+    const int j = tid;
+    const uint64_t m = s_anc[j];
+    const int off = s_off[j];
+    uint64_t rest = m;
+    while (rest) {
+      const int an = __builtin_ctzll(rest);
+      rest &= rest - 1ull;
+      const int ta = s_depth[an] - 1;
+      uint64_t from = m & ~((1ull << an) - 1ull);
+      float s = 0.f;
+      while (from) {
+        const int e = __builtin_ctzll(from);
+        from &= from - 1ull;
+        s = __builtin_fmaf(lq[off + s_depth[e] - 1], tl[s_off[e] + ta], s);
+      }
+      ml[off + ta] = s;
+    }
+  }
+  __syncthreads();
+
+  // ---- U = T R and M R on the matrix cores; A fragments (rows j, 4
+  //      consecutive columns a) are expanded from the compact lists.
+  if (!cols_live) return;
+  s16x4 rhi[NT], rlo[NT];
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
+  f32x4 uacc[NT], oacc[NT];
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt) {
+    uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    oacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const int j = mt * 16 + lc;  // A-fragment row
+    if (mt * 16 >= n) continue;
+    const bool jl = j < n;
+    const uint64_t m = jl ? s_anc[j] : 0ull;
+    const int off = jl ? s_off[j] : 0;
+#pragma unroll
+    for (int ks = 0; ks <= mt; ++ks) {
+      float tv[4], mv[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int an = ks * 16 + 4 * lg + e;
+        const bool on = (m >> an) & 1ull;
+        const int idx = on ? off + s_depth[an] - 1 : 0;
+        tv[e] = on ? tl[idx] : 0.f;
+        mv[e] = on ? ml[idx] : 0.f;
+      }
+      s16x4 thi, tlo, mhi, mlo;
+      split4(tv, thi, tlo);
+      split4(mv, mhi, mlo);
+      uacc[mt] = mfma16(thi, rhi[ks], uacc[mt]);
+      uacc[mt] = mfma16(thi, rlo[ks], uacc[mt]);
+      uacc[mt] = mfma16(tlo, rhi[ks], uacc[mt]);
+      oacc[mt] = mfma16(mhi, rhi[ks], oacc[mt]);
+      oacc[mt] = mfma16(mhi, rlo[ks], oacc[mt]);
+      oacc[mt] = mfma16(mlo, rhi[ks], oacc[mt]);
+    }
+  }
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = mt * 16 + 4 * lg + r;
+      if (j >= n) continue;
+      const size_t o = ((nbase + j) * H + h) * dv + col;
+      a.fu[o] = uacc[mt][r];
+      a.out[o] = __builtin_fmaf(s_gamma[j], pacc[mt][r], oacc[mt][r]);
+    }
 }
 
 constexpr size_t kMaxLds = 160 * 1024;
