@@ -119,9 +119,10 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
   } else if (route == SLA_ROUTE_SERIAL) {
     use_parallel = false;
   } else {
-    // Chains keep the state tile resident and advance it in place; branching
-    // drafts go to the tree-masked contraction when the shape allows it.
-    use_parallel = !chain && sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype);
+    // bf16 drafts, chains included, go to the tree-masked contraction on the
+    // matrix cores (its one dense contraction streams the state better than
+    // per-node reductions do); fp32 activations stay on the serial route.
+    use_parallel = sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype);
   }
 
   sla::VerifyArgs a;

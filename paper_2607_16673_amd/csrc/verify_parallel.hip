@@ -9,28 +9,31 @@
 //     O = Gamma Q H0 + Attn U,   Attn_ja = D_ja (q_j . k_a)   for a in P(j)
 // which is the tree-masked UT form: T = (I + Lk)^-1 is the paper's
 // T_tree = solve_tril(I - A_tree), and O = Q^ S0^T - Attn W S0^T + Attn U.
-// Here both per-column products are taken from R:
-//     U = T R,     O = Gamma P_q + M R,     M = Attn T,
-// so the only sequential work is the small per-unit T and M (each lane walks
-// its own node's root path), and everything that scales with the state's
-// columns runs on the matrix cores.  Only the committed state is read.
+// Both per-column products run on the matrix cores:
+//     U = T R,      O = Gamma P_q + Attn U,
+// and the only sequential work is the small per-unit T (each lane walks its
+// own node's root path).  Only the committed state is read.
 //
 // One workgroup = one (batch b, head h, 64-column V-tile); four wavefronts of
 // 16 state columns each.
-//   setup   wave 0: topology, decays gamma, compact-list offsets;
-//           wave 1: validates the pending accepted path and stages its factor
-//                   records in LDS; waves 2-3: stage [Q; K] in LDS.
-//   state   each lane loads 8 consecutive rows of one column per 32-row
+//   setup   all global reads that do not depend on another read are issued
+//           first (state tile, parent row, gates, path row, [Q; K], values);
+//           wave 0 builds topology, decays and offsets; wave 1 validates the
+//           pending accepted path and stages its factor records in LDS (one
+//           more dependent level); waves 2-3 stage [Q; K] in LDS.
+//   state   each lane holds 8 consecutive rows of one column per 32-row
 //           K-step (the B fragment of v_mfma_f32_16x16x32_bf16), applies the
 //           pending path, writes the committed tile back, splits fp32 into
 //           bf16 hi + lo.
 //   P       [Q; K] H0 on the matrix cores (q, k exact in bf16).
-//   Gram    [Q; K] K^T tiles that hold ancestor pairs (exact products); the
-//           ancestor entries go to per-node compact lists (ordered by depth).
-//   T, M    per node, along its root path, in fp32 on the vector ALUs.
-//   U, O    T R and M R with v_mfma_f32_16x16x16bf16_1k, whose B fragment
-//           is exactly the accumulator layout that holds R; fp32 operands
-//           enter as bf16 hi + lo (three products).
+//   Gram    [Q; K] K^T tiles that hold ancestor pairs (exact products); Attn
+//           goes to a dense LDS matrix, Lk to per-node compact lists.
+//   T       per node along its root path, fp32, into a dense LDS matrix.
+//   U, O    v_mfma_f32_16x16x16bf16_1k, whose B fragment is exactly the
+//           accumulator layout that holds R (and then U); fp32 operands enter
+//           as bf16 hi + lo (three products).
+// The state tile and the per-node outputs are streamed once, with
+// non-temporal hints.
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -49,15 +52,17 @@ constexpr int kPMax = 8;                       // pending steps staged in LDS
 
 template <int DK, int NP>
 struct Lds {
-  static constexpr int XP = DK + 8;                   // bf16 row pitch of [Q; K]
-  static constexpr int kList = NP * (NP + 1) / 2;     // compact list capacity (floats)
+  static constexpr int XP = DK + 8;                  // bf16 row pitch of [Q; K]
+  static constexpr int DP = NP + 4;                  // fp32 row pitch of dense T and Attn
+  static constexpr int kList = NP * (NP + 1) / 2;    // compact Lk capacity (floats)
   static constexpr int kXBytes = 2 * NP * XP * 2;
-  static constexpr int kListBytes = 4 * kList * 4;    // Lk, Lq, T, M
-  static constexpr int kA = kXBytes > kListBytes ? kXBytes : kListBytes;  // [Q; K], later the lists
+  static constexpr int kDenseBytes = 2 * NP * DP * 4;
+  static constexpr int kA = kXBytes > kDenseBytes ? kXBytes : kDenseBytes;  // [Q; K], then T and Attn
+  static constexpr int kLk = kList * 4;
   static constexpr int kPk = kPMax * DK * 2;          // pending keys (bf16)
   static constexpr int kPu = kPMax * kTileCols * 4;   // pending corrected values of this tile
-  static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 8 + 16;
-  static constexpr int kBytes = kA + kPk + kPu + kTopo;
+  static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 4 + 16;
+  static constexpr int kBytes = kA + kLk + kPk + kPu + kTopo;
 };
 
 __device__ __forceinline__ bf16x8 split8(const float (&x)[8], bf16x8 &lo) {
@@ -71,7 +76,7 @@ __device__ __forceinline__ bf16x8 split8(const float (&x)[8], bf16x8 &lo) {
   return hi;
 }
 
-__device__ __forceinline__ void split4(const float (&x)[4], s16x4 &hi, s16x4 &lo) {
+__device__ __forceinline__ void split4(f32x4 x, s16x4 &hi, s16x4 &lo) {
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
     const __bf16 h = static_cast<__bf16>(x[e]);
@@ -84,6 +89,14 @@ __device__ __forceinline__ f32x4 mfma16(s16x4 a, s16x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
 
+// acc += A B with A and B fp32 given as hi + lo (the lo * lo term is below
+// fp32 resolution and dropped).
+__device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x4 bl, f32x4 acc) {
+  acc = mfma16(ah, bh, acc);
+  acc = mfma16(ah, bl, acc);
+  return mfma16(al, bh, acc);
+}
+
 template <int DK, int NP>
 __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a) {
   constexpr int KS = DK / 32;  // K-steps of the contraction over d_k
@@ -94,23 +107,21 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
   using L = Lds<DK, NP>;
 
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  __bf16 *xs = reinterpret_cast<__bf16 *>(lds);            // [2NP][XP], phase 1
-  float *lk = reinterpret_cast<float *>(lds);              // compact lists, phase 2
-  float *lq = lk + L::kList;
-  float *tl = lq + L::kList;
-  float *ml = tl + L::kList;
-  __bf16 *s_pk = reinterpret_cast<__bf16 *>(lds + L::kA);  // [kPMax][DK]
-  float *s_pu = reinterpret_cast<float *>(lds + L::kA + L::kPk);  // [kPMax][64]
-  unsigned char *tp = lds + L::kA + L::kPk + L::kPu;
+  __bf16 *xs = reinterpret_cast<__bf16 *>(lds);                  // [2NP][XP] until the Grams are done
+  float *tdn = reinterpret_cast<float *>(lds);                   // [NP][DP] T, afterwards
+  float *adn = tdn + NP * L::DP;                                 // [NP][DP] Attn, afterwards
+  float *lk = reinterpret_cast<float *>(lds + L::kA);            // compact Lk
+  __bf16 *s_pk = reinterpret_cast<__bf16 *>(lds + L::kA + L::kLk);          // [kPMax][DK]
+  float *s_pu = reinterpret_cast<float *>(lds + L::kA + L::kLk + L::kPk);   // [kPMax][64]
+  unsigned char *tp = lds + L::kA + L::kLk + L::kPk + L::kPu;
   uint64_t *s_anc = reinterpret_cast<uint64_t *>(tp);      // [NP]
   int *s_depth = reinterpret_cast<int *>(tp + 8 * NP);     // [NP]
   int *s_off = s_depth + NP;                                // [NP]
   float *s_gamma = reinterpret_cast<float *>(s_off + NP);  // [NP]
   float *s_rgamma = s_gamma + NP;                           // [NP] 1 / gamma
   float *s_be = s_rgamma + NP;                              // [NP]
-  int *s_pnode = reinterpret_cast<int *>(s_be + NP);        // [kPMax]
-  float *s_palpha = reinterpret_cast<float *>(s_pnode + kPMax);  // [kPMax]
-  int *s_misc = reinterpret_cast<int *>(s_palpha + kPMax);  // topo err, max depth, path err, path len
+  float *s_palpha = s_be + NP;                              // [kPMax]
+  int *s_misc = reinterpret_cast<int *>(s_palpha + kPMax);  // topo err, path err, path len
 
   const int tid = threadIdx.x;
   const int w = tid / kWave;
@@ -133,8 +144,8 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
   const bf16 *kg = static_cast<const bf16 *>(a.k);
   const bf16 *vg = static_cast<const bf16 *>(a.v);
 
-  // ---- independent loads first: the state tile (the only state read) and
-  //      the values of the nodes whose accumulator rows this lane holds.
+  // ---- reads with no dependence on other reads: the state tile (the only
+  //      state read) and the values of the nodes this lane solves for
   float *st = a.state + unit * DK * dv + col;
   float hf[KS][8];
   float vreg[NT][4];
@@ -142,7 +153,7 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) hf[ks][e] = st[(size_t)(ks * 32 + 8 * lg + e) * dv];
+      for (int e = 0; e < 8; ++e) hf[ks][e] = __builtin_nontemporal_load(st + (size_t)(ks * 32 + 8 * lg + e) * dv);
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
@@ -156,14 +167,14 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
   if (w == 0) {
     // topology, decays and compact-list offsets; lane j owns node j
     const bool live = l < n;
+    const size_t s = (nbase + (live ? l : 0)) * H + h;
     const int p = live ? a.parent[nbase + l] : -1;
+    const float al = live ? a.alpha[s] : 1.f;
+    const float be = live ? a.beta[s] : 0.f;
     bool bad = live && (p < -1 || p >= l);
     if (a.chain) bad = bad || (live && p != l - 1);
     const int err = wave_any(bad) ? SLA_ERR_TOPOLOGY : SLA_OK;
     if (err == SLA_OK) {
-      const size_t s = ((nbase + (live ? l : 0)) * H + h);
-      const float al = live ? a.alpha[s] : 1.f;
-      const float be = live ? a.beta[s] : 0.f;
       uint64_t m = live ? (1ull << l) : 0ull;
       float g = al;
       int d = live ? 1 : 0;
@@ -179,15 +190,12 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
         }
         x = x >= 0 ? px : -1;
       }
-      int incl = d;  // inclusive prefix sum of depths -> list offsets
+      int incl = d;  // inclusive prefix sum of depths -> compact-list offsets
 #pragma unroll
       for (int o = 1; o < kWave; o <<= 1) {
         const int y = __shfl_up(incl, o);
         if (l >= o) incl += y;
       }
-      int md = d;
-#pragma unroll
-      for (int o = 1; o < kWave; o <<= 1) md = max(md, __shfl_xor(md, o));
       if (live) {
         s_anc[l] = m;
         s_depth[l] = d;
@@ -196,40 +204,47 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
         s_rgamma[l] = 1.f / g;
         s_be[l] = be;
       }
-      if (l == 0) s_misc[1] = md;
     }
     if (l == 0) s_misc[0] = err;
   } else if (w == 1) {
-    // pending accepted path: validate, then stage its records in LDS
+    // pending accepted path: validate and stage its records in LDS.  The
+    // path row and its length are read together; the records they name are
+    // the one dependent level.
     int perr = SLA_OK, plen = 0;
     if (a.has_pending) {
       const int pn = a.pend.n;
+      const int32_t *prow = a.pend.path + (size_t)b * pn;
       plen = a.pend.len[b];
-      perr = check_path(a.pend.parent + (size_t)b * pn, pn, a.pend.path + (size_t)b * pn, plen, l);
+      const int node = l < pn ? prow[l] : -1;
+      const int prev = l == 0 ? -1 : (l - 1 < pn ? prow[l - 1] : -1);
+      const bool step = l < plen;
+      const bool inrange = node >= 0 && node < pn;
+      const int ppar = (step && inrange) ? a.pend.parent[(size_t)b * pn + node] : -2;
+      const bool bad = (plen < 0 || plen > pn) || (step && (!inrange || ppar != prev));
+      perr = wave_any(bad) ? SLA_ERR_PATH : SLA_OK;
       if (perr == SLA_OK) {
         const int ps = plen < kPMax ? plen : kPMax;
-        if (l < ps) {
-          const int node = a.pend.path[(size_t)b * pn + l];
-          s_pnode[l] = node;
-          s_palpha[l] = a.pend.alpha[((size_t)b * pn + node) * H + h];
-        }
-        __builtin_amdgcn_wave_barrier();
+        if (l < ps) s_palpha[l] = a.pend.alpha[((size_t)b * pn + node) * H + h];
         const bf16 *pk = static_cast<const bf16 *>(a.pend.k);
-        for (int c = l; c < ps * CH; c += kWave) {
+        const int iters = (ps * CH + kWave - 1) / kWave;
+        for (int it = 0; it < iters; ++it) {
+          const int c = l + it * kWave;
           const int t = c / CH, part = c % CH;
-          const size_t src = (((size_t)b * pn + s_pnode[t]) * H + h) * DK + part * 8;
-          *reinterpret_cast<uint4 *>(s_pk + t * DK + part * 8) = *reinterpret_cast<const uint4 *>(pk + src);
+          const int nt = __shfl(node, t < ps ? t : 0);
+          if (c < ps * CH)
+            *reinterpret_cast<uint4 *>(s_pk + t * DK + part * 8) =
+                *reinterpret_cast<const uint4 *>(pk + (((size_t)b * pn + nt) * H + h) * DK + part * 8);
         }
+        const int cg = tile * kTileCols + l;
         for (int t = 0; t < ps; ++t) {
-          const int cg = tile * kTileCols + l;
-          s_pu[t * kTileCols + l] =
-              cg < dv ? a.pend.u[(((size_t)b * pn + s_pnode[t]) * H + h) * dv + cg] : 0.f;
+          const int nt = __builtin_amdgcn_readlane(node, t);
+          s_pu[t * kTileCols + l] = cg < dv ? a.pend.u[(((size_t)b * pn + nt) * H + h) * dv + cg] : 0.f;
         }
       }
     }
     if (l == 0) {
-      s_misc[2] = perr;
-      s_misc[3] = plen;
+      s_misc[1] = perr;
+      s_misc[2] = plen;
     }
   } else {
     // [Q; K]: rows 0..NP-1 hold q_j, rows NP..2NP-1 hold k_j; zero padding
@@ -242,10 +257,10 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
     }
   }
   __syncthreads();
-  const int err = s_misc[0] != SLA_OK ? s_misc[0] : s_misc[2];
+  const int err = s_misc[0] != SLA_OK ? s_misc[0] : s_misc[1];
   if (tile == 0 && h == 0 && tid == 0 && a.status) a.status[b] = err;
   if (err != SLA_OK) return;
-  const int plen = s_misc[3];
+  const int plen = s_misc[2];
 
   // ---- factor records that do not depend on the V-tile
   if (tile == 0) {
@@ -296,7 +311,7 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-        for (int e = 0; e < 8; ++e) st[(size_t)(ks * 32 + 8 * lg + e) * dv] = hf[ks][e];
+        for (int e = 0; e < 8; ++e) __builtin_nontemporal_store(hf[ks][e], st + (size_t)(ks * 32 + 8 * lg + e) * dv);
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) bhi[ks] = split8(hf[ks], blo[ks]);
@@ -341,10 +356,25 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
         }
       }
   }
-  __syncthreads();  // [Q; K] is dead from here on; its space holds the lists
+  __syncthreads();  // [Q; K] is dead from here on; its space holds T and Attn
 
-  // ---- scatter ancestor entries of the Grams into the compact lists:
-  //      entry (j, a) of a list lives at off_j + depth(a) - 1
+  // ---- zero the dense T and Attn (rows of padding nodes stay zero)
+  for (int c = tid; c < 2 * NP * L::DP / 4; c += kThreads)
+    reinterpret_cast<float4 *>(tdn)[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+
+  // ---- R = beta (v - gamma P_k) in the accumulator layout
+  f32x4 rreg[NT];
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int j = mt * 16 + 4 * lg + r;
+      rreg[mt][r] = (cols_live && j < n) ? s_be[j] * (vreg[mt][r] - s_gamma[j] * pacc[NT + mt][r]) : 0.f;
+    }
+  __syncthreads();
+
+  // ---- scatter ancestor entries of the Grams: Attn into its dense matrix,
+  //      Lk into the compact list of node j at off_j + depth(a) - 1
   {
     int tc = 0;
 #pragma unroll
@@ -357,37 +387,24 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
         for (int r = 0; r < 4; ++r) {
           const int j = (mr % NT) * 16 + 4 * lg + r;
           if (j >= n || an > j) continue;
-          const uint64_t m = s_anc[j];
-          if (!((m >> an) & 1ull)) continue;
-          const int idx = s_off[j] + s_depth[an] - 1;
-          const float dja = s_gamma[j] * s_rgamma[an];
-          const float gv = gacc[tc / kWaves][r];
+          if (!((s_anc[j] >> an) & 1ull)) continue;
+          const float dg = s_gamma[j] * s_rgamma[an] * gacc[tc / kWaves][r];
           if (mr < NT)
-            lq[idx] = dja * gv;
+            adn[j * L::DP + an] = dg;
           else if (an < j)
-            lk[idx] = s_be[j] * dja * gv;
+            lk[s_off[j] + s_depth[an] - 1] = s_be[j] * dg;
         }
       }
   }
+  __syncthreads();
 
-  // ---- R = beta (v - gamma P_k) in the accumulator layout
-  float rreg[NT][4];
-#pragma unroll
-  for (int mt = 0; mt < NT; ++mt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int j = mt * 16 + 4 * lg + r;
-      rreg[mt][r] = (cols_live && j < n) ? s_be[j] * (vreg[mt][r] - s_gamma[j] * pacc[NT + mt][r]) : 0.f;
-    }
-  __syncthreads();  // lists complete
-
-  // ---- T = (I + Lk)^-1, row j along P(j) (deepest ancestor first):
+  // ---- T = (I + Lk)^-1, row j along P(j), deepest ancestor first:
   //      T_jj = 1,  T_ja = - sum_{e in P(j), a < e} T_je Lk_ea
   if (tid < n) {
     const int j = tid;
     const uint64_t m = s_anc[j];
-    const int off = s_off[j];
-    tl[off + s_depth[j] - 1] = 1.f;
+    float *trow = tdn + j * L::DP;
+    trow[j] = 1.f;
     uint64_t rest = m & ~(1ull << j);
     while (rest) {
       const int an = 63 - __builtin_clzll(rest);
@@ -398,71 +415,46 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
       while (below) {
         const int e = __builtin_ctzll(below);
         below &= below - 1ull;
-        s = __builtin_fmaf(-tl[off + s_depth[e] - 1], lk[s_off[e] + ta], s);
+        s = __builtin_fmaf(-trow[e], lk[s_off[e] + ta], s);
       }
-      tl[off + ta] = s;
+      trow[an] = s;
     }
   }
   __syncthreads();
 
-  // ---- M = Attn T, row j:  M_ja = sum_{e in P(j), a <= e} Attn_je T_ea
-  if (tid < n) {
-    const int j = tid;
-    const uint64_t m = s_anc[j];
-    const int off = s_off[j];
-    uint64_t rest = m;
-    while (rest) {
-      const int an = __builtin_ctzll(rest);
-      rest &= rest - 1ull;
-      const int ta = s_depth[an] - 1;
-      uint64_t from = m & ~((1ull << an) - 1ull);
-      float s = 0.f;
-      while (from) {
-        const int e = __builtin_ctzll(from);
-        from &= from - 1ull;
-        s = __builtin_fmaf(lq[off + s_depth[e] - 1], tl[s_off[e] + ta], s);
-      }
-      ml[off + ta] = s;
-    }
-  }
-  __syncthreads();
-
-  // ---- U = T R and M R on the matrix cores; A fragments (rows j, 4
-  //      consecutive columns a) are expanded from the compact lists.
+  // ---- U = T R, then O = Gamma P_q + Attn U, on the matrix cores; A
+  //      fragments are rows j = 16 mt + lc, columns 16 ks + 4 lg .. + 3
   if (!cols_live) return;
   s16x4 rhi[NT], rlo[NT];
 #pragma unroll
   for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
-  f32x4 uacc[NT], oacc[NT];
+  f32x4 uacc[NT];
 #pragma unroll
   for (int mt = 0; mt < NT; ++mt) {
     uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    oacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    const int j = mt * 16 + lc;  // A-fragment row
     if (mt * 16 >= n) continue;
-    const bool jl = j < n;
-    const uint64_t m = jl ? s_anc[j] : 0ull;
-    const int off = jl ? s_off[j] : 0;
 #pragma unroll
     for (int ks = 0; ks <= mt; ++ks) {
-      float tv[4], mv[4];
+      const f32x4 tv = *reinterpret_cast<const f32x4 *>(tdn + (mt * 16 + lc) * L::DP + ks * 16 + 4 * lg);
+      s16x4 th, tlo;
+      split4(tv, th, tlo);
+      uacc[mt] = mfma16_split(th, tlo, rhi[ks], rlo[ks], uacc[mt]);
+    }
+  }
+  s16x4 uhi[NT], ulo[NT];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int an = ks * 16 + 4 * lg + e;
-        const bool on = (m >> an) & 1ull;
-        const int idx = on ? off + s_depth[an] - 1 : 0;
-        tv[e] = on ? tl[idx] : 0.f;
-        mv[e] = on ? ml[idx] : 0.f;
-      }
-      s16x4 thi, tlo, mhi, mlo;
-      split4(tv, thi, tlo);
-      split4(mv, mhi, mlo);
-      uacc[mt] = mfma16(thi, rhi[ks], uacc[mt]);
-      uacc[mt] = mfma16(thi, rlo[ks], uacc[mt]);
-      uacc[mt] = mfma16(tlo, rhi[ks], uacc[mt]);
-      oacc[mt] = mfma16(mhi, rhi[ks], oacc[mt]);
-      oacc[mt] = mfma16(mhi, rlo[ks], oacc[mt]);
-      oacc[mt] = mfma16(mlo, rhi[ks], oacc[mt]);
+  for (int mt = 0; mt < NT; ++mt) split4(uacc[mt], uhi[mt], ulo[mt]);
+  f32x4 oacc[NT];
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt) {
+    oacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (mt * 16 >= n) continue;
+#pragma unroll
+    for (int ks = 0; ks <= mt; ++ks) {
+      const f32x4 av = *reinterpret_cast<const f32x4 *>(adn + (mt * 16 + lc) * L::DP + ks * 16 + 4 * lg);
+      s16x4 ah, alo;
+      split4(av, ah, alo);
+      oacc[mt] = mfma16_split(ah, alo, uhi[ks], ulo[ks], oacc[mt]);
     }
   }
 #pragma unroll
@@ -472,8 +464,8 @@ __global__ __launch_bounds__(kThreads) void verify_parallel_kernel(VerifyArgs a)
       const int j = mt * 16 + 4 * lg + r;
       if (j >= n) continue;
       const size_t o = ((nbase + j) * H + h) * dv + col;
-      a.fu[o] = uacc[mt][r];
-      a.out[o] = __builtin_fmaf(s_gamma[j], pacc[mt][r], oacc[mt][r]);
+      __builtin_nontemporal_store(uacc[mt][r], a.fu + o);
+      __builtin_nontemporal_store(__builtin_fmaf(s_gamma[j], pacc[mt][r], oacc[mt][r]), a.out + o);
     }
 }
 
