@@ -86,6 +86,8 @@ def main():
     ap.add_argument("--separate", action="store_true",
                     help="time the separate route (verify, then standalone commit) instead of the fused one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", dest="graph", action="store_false",
+                    help="launch eagerly from Python with HIP events around every launch")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters (if present)")
     args = ap.parse_args()
@@ -161,37 +163,74 @@ def main():
         step_no[0] += 1
 
     log("bench: warmup %d" % args.warmup)
-    for _ in range(max(args.warmup, 1)):
+    for _ in range(max(args.warmup, 2)):
         step()
     torch.cuda.synchronize()
     assert int(status.abs().max()) == 0, "device reported a data error"
 
-    log("bench: timing %d steps" % args.steps)
-    events = []
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(events)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    elapsed = t1 - t0
-    ms_per_step = 1e3 * elapsed / args.steps
-
-    # verify-kernel durations from the HIP events bracketing each launch
-    if args.separate:
-        per = 3
-        vdur = [events[i].elapsed_time(events[i + 1]) for i in range(0, len(events), per)]
-        cdur = [events[i + 1].elapsed_time(events[i + 2]) for i in range(0, len(events), per)]
-    else:
-        vdur = [events[i].elapsed_time(events[i + 1]) for i in range(0, len(events), 2)]
+    launches_per_step = cfg.layers * (2 if args.separate else 1)
+    if args.graph:
+        # One graph holds two consecutive steps (the factor stores ping-pong),
+        # replayed back to back: no host work between kernel launches.
+        if step_no[0] % 2:
+            step()
+        g = torch.cuda.CUDAGraph()
+        s_cap = torch.cuda.Stream(dev)
+        s_cap.wait_stream(stream)
+        with torch.cuda.stream(s_cap):
+            with torch.cuda.graph(g, stream=s_cap):
+                for _ in range(2):
+                    step()
+        torch.cuda.synchronize()
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        reps = max(1, args.steps // 2)
+        steps = 2 * reps
+        log("bench: timing %d steps (graph replays)" % steps)
+        cur = torch.cuda.current_stream(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        e0.record(cur)
+        for _ in range(reps):
+            g.replay()
+        e1.record(cur)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        elapsed = t1 - t0
+        # launches in a graph run back to back: the mean launch duration is the
+        # event-timed replay span over the launches it holds
+        vdur = [e0.elapsed_time(e1) / (steps * launches_per_step)]
         cdur = []
+    else:
+        steps = args.steps
+        log("bench: timing %d steps" % steps)
+        events = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step(events)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        elapsed = t1 - t0
+        # verify-kernel durations from the HIP events bracketing each launch
+        if args.separate:
+            per = 3
+            vdur = [events[i].elapsed_time(events[i + 1]) for i in range(0, len(events), per)]
+            cdur = [events[i + 1].elapsed_time(events[i + 2]) for i in range(0, len(events), per)]
+        else:
+            vdur = [events[i].elapsed_time(events[i + 1]) for i in range(0, len(events), 2)]
+            cdur = []
+    assert int(status.abs().max()) == 0, "device reported a data error"
+    ms_per_step = 1e3 * elapsed / steps
     v_ms = float(np.mean(vdur))
     bytes_launch = algorithmic_bytes(cfg, rnd.length)
     if args.separate:
         # without a pending path the verify reads the state only; commit reads and writes it
         bytes_launch -= cfg.batch * cfg.heads * cfg.d_k * cfg.d_v * 4
     achieved = bytes_launch / (v_ms * 1e-3) / 1e9
-    nodes = cfg.batch * cfg.n_nodes * cfg.layers * args.steps
+    nodes = cfg.batch * cfg.n_nodes * cfg.layers * steps
     value = nodes / elapsed
     traffic = None
     kernel = None
@@ -207,14 +246,15 @@ def main():
             "kernel": kernel or "sla verify (%s route)" % args.route,
             "algorithmic_bytes_per_launch": int(bytes_launch), "avg_launch_ms": round(v_ms, 5)}
     line = {
-        "metric": METRIC, "value": round(value, 1), "unit": "nodes/s", "n_gpus": 1, "steps": args.steps,
+        "metric": METRIC, "value": round(value, 1), "unit": "nodes/s", "n_gpus": 1, "steps": steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
         "config": {"workload": cfg.name, "batch": cfg.batch, "heads": cfg.heads, "d_k": cfg.d_k,
                    "d_v": cfg.d_v, "nodes_per_tree": cfg.n_nodes, "topology": topo,
                    "max_depth": cfg.max_depth, "max_branch": cfg.max_branch, "layers": cfg.layers,
                    "qkv_dtype": cfg.dtype, "state_dtype": "f32", "route": args.route,
-                   "commit": "separate" if args.separate else "fused", "parallelism": "single-gpu"},
+                   "commit": "separate" if args.separate else "fused", "parallelism": "single-gpu",
+                   "launch": "hip graph" if args.graph else "eager"},
         "hbm_gbps": round(achieved, 1),
         "roofline": roof,
     }

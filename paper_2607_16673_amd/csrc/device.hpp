@@ -51,6 +51,36 @@ __device__ __forceinline__ void load_f32(const bf16 *__restrict__ p, float (&out
   }
 }
 
+// ------------------------------------------------------ buffer resources
+// Raw buffer descriptors: a 128-bit base/size descriptor in scalar
+// registers, a per-lane 32-bit VGPR offset and a wave-uniform SGPR offset.
+// Strided accesses then cost one VGPR per lane instead of a 64-bit address
+// per access.  Reads at offsets >= the descriptor's byte count return zero
+// and writes there are dropped.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kBufWord3 = 0x00020000;  // raw 32-bit dword access, no swizzle
+constexpr int kPolicyDefault = 0;
+constexpr int kPolicyStream = 2;  // non-temporal: data touched once
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, kBufWord3);
+}
+
+template <int POLICY>
+__device__ __forceinline__ float buf_load_f32(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, POLICY));
+}
+
+template <int POLICY>
+__device__ __forceinline__ void buf_store_f32(float x, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, voff, soff, POLICY);
+}
+
+// one bf16 activation, widened to fp32
+__device__ __forceinline__ float buf_load_bf16(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, kPolicyDefault) << 16);
+}
+
 // ------------------------------------------------------- rank-one update
 // One accepted (or materialised) node a advances the transposed state
 // H = S^T elementwise:  H[i][c] <- alpha_a * H[i][c] + k_a[i] * u_a[c].

@@ -1,0 +1,519 @@
+// verify_tile.hip -- tree-masked factorised verification (SpecLA §4.2) with
+// the delayed state update of §5.2 fused in front of it.
+//
+// Unrolling the gated delta rule along a root path gives, for every node j
+// (gamma_j = product of alpha over P(j), D_ja = gamma_j / gamma_a, a in P(j)):
+//     H_j = gamma_j H0 + sum_{a in P(j)} D_ja k_a u_a^T
+//     (I + Lk) U = R,   R_j = beta_j (v_j - gamma_j H0^T k_j),
+//                       Lk_ja = beta_j D_ja (k_j . k_a)   for a in P(j), a != j
+//     O = Gamma Q H0 + Attn U,   Attn_ja = D_ja (q_j . k_a)   for a in P(j)
+// which is the tree-masked UT form: T = (I + Lk)^-1 is the paper's
+// T_tree = solve_tril(I - A_tree), and O = Q^ S0^T - Attn W S0^T + Attn U.
+// Both per-column products run on the matrix cores:
+//     U = T R,      O = Gamma P_q + Attn U,
+// and the only sequential work is the small per-unit T (each lane walks its
+// own node's root path).  Only the committed state is read.
+//
+// One workgroup = one (batch b, head h, 64-column V-tile), five wavefronts:
+//   waves 0-3  own 16 state columns each.  They issue the state tile reads
+//              (non-temporal, in the B-fragment order of
+//              v_mfma_f32_16x16x32_bf16: 8 consecutive rows of one column per
+//              32-row K-step) and the value reads first thing, and consume the
+//              tile K-step by K-step as it lands: pending path applied,
+//              committed rows written back, fp32 split into bf16 hi + lo,
+//              P = [Q; K] H0 accumulated on the matrix cores.  Then
+//              R = beta (v - gamma P_k), U = T R and O = Gamma P_q + Attn U on
+//              v_mfma_f32_16x16x16bf16_1k (whose B fragment is exactly the
+//              accumulator layout holding R, then U), and the outputs.
+//   wave 4     owns no state.  It takes every read that depends on another
+//              read: parent row and gates -> topology, decays and compact-list
+//              offsets; pending path -> validation and the factor records it
+//              names; and it stages [Q; K] with direct global->LDS loads.
+//              After the Grams it solves the per-node rows of T.
+// The tree-masked Grams ([Q; K] K^T tiles that hold ancestor pairs, exact
+// bf16 products) are spread over all five waves; they and T are done while
+// the state tile is still in flight.  Strided global accesses go through
+// buffer descriptors (one VGPR offset per lane).
+#include "device.hpp"
+#include "kernels.hpp"
+
+namespace sla {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) short s16x4;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int kColWaves = 4;
+constexpr int kSetup = kColWaves;                // wave index of the setup wave
+constexpr int kWaves = kColWaves + 1;
+constexpr int kThreads = kWaves * kWave;         // 320
+constexpr int kWaveCols = 16;
+constexpr int kTileCols = kColWaves * kWaveCols;  // 64 state columns per workgroup
+constexpr int kPMax = 8;                          // pending steps staged in LDS
+constexpr int kBP = 20;                           // fp32 row pitch of a 16x16 block
+
+template <int DK, int NP>
+struct Layout {
+  static constexpr int NT = NP / 16, KS = DK / 32, CH = DK / 8, MT = 2 * NT;
+  static constexpr int NB = NT * (NT + 1) / 2;      // lower-triangular 16x16 blocks
+  static constexpr int kList = NP * (NP + 1) / 2;   // compact Lk capacity (floats)
+  static constexpr int kX = 2 * NP * CH * 16;       // [Q; K], 16-byte chunks, xor-swizzled
+  static constexpr int kBlk = 16 * kBP * 4;
+  static constexpr int kT = NB * kBlk;              // T blocks
+  static constexpr int kAt = NB * kBlk;             // Attn blocks
+  static constexpr int kLk = kList * 4;
+  static constexpr int kPk = kPMax * DK * 2;        // pending keys (bf16)
+  static constexpr int kPu = kPMax * kTileCols * 4; // pending corrected values of this tile
+  static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 4 + 16;
+  static constexpr int kBytes = kX + kT + kAt + kLk + kPk + kPu + kTopo;
+};
+
+// [Q; K] chunk (row, c) lives at row * CH + (c ^ (row & 7)): the 16 rows a
+// fragment read touches fall on distinct bank groups.
+template <int CH>
+__device__ __forceinline__ int xchunk(int row, int c) {
+  return row * CH + (c ^ (row & 7));
+}
+
+// Each lane's 16 bytes land at lds_wave_base + 16 * lane (the base is
+// wave-uniform); no registers are involved.
+__device__ __forceinline__ void load_lds16(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)(lds_wave_base), 16, 0, 0);
+}
+
+// element (row j, column a), a <= j, of a lower-triangular 16x16-blocked matrix
+__device__ __forceinline__ int blk(int j, int a) {
+  const int bj = j >> 4;
+  return ((bj * (bj + 1)) / 2 + (a >> 4)) * (16 * kBP) + (j & 15) * kBP + (a & 15);
+}
+
+__device__ __forceinline__ void split8(const float (&x)[8], bf16x8 &hi, bf16x8 &lo) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 h = static_cast<__bf16>(x[e]);
+    hi[e] = h;
+    lo[e] = static_cast<__bf16>(x[e] - static_cast<float>(h));
+  }
+}
+
+__device__ __forceinline__ void split4(f32x4 x, s16x4 &hi, s16x4 &lo) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const __bf16 h = static_cast<__bf16>(x[e]);
+    hi[e] = __builtin_bit_cast(short, h);
+    lo[e] = __builtin_bit_cast(short, static_cast<__bf16>(x[e] - static_cast<float>(h)));
+  }
+}
+
+__device__ __forceinline__ f32x4 mfma16(s16x4 a, s16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+// acc += A B with A and B fp32 given as hi + lo (the lo * lo term is below
+// fp32 resolution and dropped).
+__device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x4 bl, f32x4 acc) {
+  acc = mfma16(ah, bh, acc);
+  acc = mfma16(ah, bl, acc);
+  return mfma16(al, bh, acc);
+}
+
+template <int DK, int NP>
+__global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
+  using L = Layout<DK, NP>;
+  constexpr int KS = L::KS, NT = L::NT, MT = L::MT, CH = L::CH;
+  constexpr int NGT = NT * (NT + 1);                 // Gram tiles (both halves)
+  constexpr int GT = (NGT + kWaves - 1) / kWaves;    // Gram tiles per wave
+
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
+  uint4 *xs = reinterpret_cast<uint4 *>(lds);                              // [Q; K]
+  float *tb = reinterpret_cast<float *>(lds + L::kX);                      // T blocks
+  float *ab = reinterpret_cast<float *>(lds + L::kX + L::kT);              // Attn blocks
+  float *lk = reinterpret_cast<float *>(lds + L::kX + L::kT + L::kAt);     // compact Lk
+  bf16 *s_pk = reinterpret_cast<bf16 *>(lds + L::kX + L::kT + L::kAt + L::kLk);             // [kPMax][DK]
+  float *s_pu = reinterpret_cast<float *>(lds + L::kX + L::kT + L::kAt + L::kLk + L::kPk);  // [kPMax][64]
+  unsigned char *tp = lds + L::kX + L::kT + L::kAt + L::kLk + L::kPk + L::kPu;
+  uint64_t *s_anc = reinterpret_cast<uint64_t *>(tp);      // [NP]
+  int *s_depth = reinterpret_cast<int *>(tp + 8 * NP);     // [NP]
+  int *s_off = s_depth + NP;                                // [NP]
+  float *s_gamma = reinterpret_cast<float *>(s_off + NP);  // [NP]
+  float *s_rgamma = s_gamma + NP;                           // [NP] 1 / gamma
+  float *s_be = s_rgamma + NP;                              // [NP]
+  float *s_palpha = s_be + NP;                              // [kPMax]
+  int *s_misc = reinterpret_cast<int *>(s_palpha + kPMax);  // err, path len
+
+  const int tid = threadIdx.x;
+  const int w = tid / kWave;
+  const int l = tid % kWave;
+  const int lc = l & 15;  // column within a wave's 16 / row within a 16-row tile
+  const int lg = l >> 4;  // row group
+  const int H = a.H, dv = a.dv, n = a.n;
+  const int ntiles = (dv + kTileCols - 1) / kTileCols;
+  int wid = blockIdx.x;
+  const int tile = wid % ntiles;
+  wid /= ntiles;
+  const int h = wid % H;
+  const int b = wid / H;
+  const int ucol = w * kWaveCols + lc;  // column within the tile
+  const int col = tile * kTileCols + ucol;
+  const bool cols_live = w < kColWaves && tile * kTileCols + w * kWaveCols < dv;  // wave-uniform
+  const size_t unit = (size_t)b * H + h;
+  const size_t nbase = (size_t)b * n;
+  const rsrc_t sr = make_rsrc(a.state + unit * DK * dv, (uint32_t)DK * dv * 4);
+  const uint32_t sv = (uint32_t)(8 * lg * dv + col) * 4;
+  const uint32_t nstride = (uint32_t)H * dv;  // elements between consecutive nodes of a unit
+
+  // ---- column waves: the state tile and the values, issued first
+  float hf[KS][8];
+  uint32_t vraw[NT][4];  // bf16 bit patterns, widened where they are used
+  if (cols_live) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) hf[ks][e] = buf_load_f32<kPolicyStream>(sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
+    // node j = 16 mt + 4 lg + q; rows past the last node fall outside the
+    // descriptor and read zero
+    const rsrc_t vr = make_rsrc(static_cast<const bf16 *>(a.v) + (nbase * H + h) * dv,
+                                ((uint32_t)(n - 1) * nstride + dv) * 2);
+    const uint32_t vv = (4 * lg * nstride + col) * 2;
+#pragma unroll
+    for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        vraw[mt][q] = __builtin_amdgcn_raw_buffer_load_b16(vr, vv + (uint32_t)(mt * 16 + q) * nstride * 2, 0, kPolicyDefault);
+  }
+
+  // ---- setup wave: everything that depends on another read
+  int p = -1;      // setup wave, lane j: parent of node j
+  float al = 1.f;  // setup wave, lane j: alpha_j
+  if (w == kSetup) {
+    const bf16 *qg = static_cast<const bf16 *>(a.q);
+    const bf16 *kg = static_cast<const bf16 *>(a.k);
+    const bool live = l < n;
+    const size_t s = (nbase + (live ? l : 0)) * H + h;
+    p = live ? a.parent[nbase + l] : -1;
+    al = live ? a.alpha[s] : 1.f;
+    const float be = live ? a.beta[s] : 0.f;
+    int plen = 0, node = -1, prev = -1;
+    const int pn = a.has_pending ? a.pend.n : 1;
+    if (a.has_pending) {
+      const int32_t *prow = a.pend.path + (size_t)b * pn;
+      plen = a.pend.len[b];
+      node = l < pn ? prow[l] : -1;
+      prev = (l >= 1 && l - 1 < pn) ? prow[l - 1] : -1;
+    }
+    // [Q; K] straight into LDS (rows 0..NP-1: q_j, NP..2NP-1: k_j; padding
+    // rows repeat node 0 and are never used)
+#pragma unroll 1
+    for (int i = 0; i < 2 * NP * CH / kWave; ++i) {
+      const int P = i * kWave + l;
+      const int row = P / CH, c = (P % CH) ^ (row & 7);
+      const int j = row % NP;
+      load_lds16((row < NP ? qg : kg) + ((nbase + (j < n ? j : 0)) * H + h) * DK + c * 8, xs + i * kWave);
+    }
+    for (int c = l; c < (L::kT + L::kAt) / 16; c += kWave) reinterpret_cast<uint4 *>(tb)[c] = make_uint4(0, 0, 0, 0);
+
+    // topology, decays and compact-list offsets; lane j owns node j
+    bool bad = live && (p < -1 || p >= l);
+    if (a.chain) bad = bad || (live && p != l - 1);
+    int err = wave_any(bad) ? SLA_ERR_TOPOLOGY : SLA_OK;
+    if (err == SLA_OK) {
+      uint64_t m = live ? (1ull << l) : 0ull;
+      float g = al;
+      int d = live ? 1 : 0;
+      int x = p;
+      while (wave_any(x >= 0)) {
+        const int src = x >= 0 ? x : 0;
+        const float ax = __shfl(al, src);
+        const int px = __shfl(p, src);
+        if (x >= 0) {
+          m |= 1ull << x;
+          g *= ax;
+          ++d;
+        }
+        x = x >= 0 ? px : -1;
+      }
+      int incl = d;  // inclusive prefix sum of depths -> compact-list offsets
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) {
+        const int y = __shfl_up(incl, o);
+        if (l >= o) incl += y;
+      }
+      if (live) {
+        s_anc[l] = m;
+        s_depth[l] = d;
+        s_off[l] = incl - d;
+        s_gamma[l] = g;
+        s_rgamma[l] = 1.f / g;
+        s_be[l] = be;
+      }
+    }
+    // pending accepted path: validate (one dependent read) and stage records
+    if (err == SLA_OK && a.has_pending) {
+      const bool step = l < plen;
+      const bool inrange = node >= 0 && node < pn;
+      const size_t srec = ((size_t)b * pn + (inrange ? node : 0)) * H + h;
+      const int ppar = (step && inrange) ? a.pend.parent[(size_t)b * pn + node] : -2;
+      const float pal = (step && inrange) ? a.pend.alpha[srec] : 0.f;
+      const bool pbad = (plen < 0 || plen > pn) || (step && (!inrange || ppar != prev));
+      err = wave_any(pbad) ? SLA_ERR_PATH : SLA_OK;
+      if (err == SLA_OK) {
+        const int ps = plen < kPMax ? plen : kPMax;
+        if (l < kPMax) s_palpha[l] = l < ps ? pal : 0.f;
+        const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
+#pragma unroll
+        for (int i = 0; i < kPMax * CH / kWave; ++i) {
+          const int P = i * kWave + l;
+          const int t = P / CH, c = P % CH;
+          const int nt = __shfl(node, t);
+          load_lds16(pkg + (t < ps ? (((size_t)b * pn + nt) * H + h) * DK + c * 8 : 0), s_pk + i * kWave * 8);
+        }
+        const int cg = tile * kTileCols + l;
+#pragma unroll
+        for (int t = 0; t < kPMax; ++t) {
+          const int nt = __builtin_amdgcn_readlane(node, t);
+          s_pu[t * kTileCols + l] =
+              (t < ps && cg < dv) ? a.pend.u[(((size_t)b * pn + nt) * H + h) * dv + cg] : 0.f;
+        }
+      }
+    }
+    if (l == 0) {
+      s_misc[0] = err;
+      s_misc[1] = plen;
+    }
+    if (tile == 0 && h == 0 && l == 0 && a.status) a.status[b] = err;
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's direct LDS loads have landed
+  }
+  __syncthreads();
+  const int err = s_misc[0];
+  if (err != SLA_OK) return;
+  const int plen = s_misc[1];
+
+  // ---- tree-masked Grams over all waves: tile (mr, na) of [Q; K] K^T holds
+  //      rows of node tile mr % NT against ancestor candidates of node tile
+  //      na <= mr % NT; ancestor entries go to Attn blocks and Lk lists
+  {
+    f32x4 gacc[GT];
+    int tc = 0;
+#pragma unroll
+    for (int mr = 0; mr < MT; ++mr)
+#pragma unroll
+      for (int na = 0; na <= mr % NT; ++na, ++tc) {
+        if (tc % kWaves != w || (mr % NT) * 16 >= n) continue;
+        f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mr * 16 + lc, ks * 4 + lg));
+          const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
+          g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, g, 0, 0, 0);
+        }
+        gacc[tc / kWaves] = g;
+      }
+    tc = 0;
+#pragma unroll
+    for (int mr = 0; mr < MT; ++mr)
+#pragma unroll
+      for (int na = 0; na <= mr % NT; ++na, ++tc) {
+        if (tc % kWaves != w || (mr % NT) * 16 >= n) continue;
+        const int an = na * 16 + lc;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = (mr % NT) * 16 + 4 * lg + q;
+          if (j >= n || an > j) continue;
+          if (!((s_anc[j] >> an) & 1ull)) continue;
+          const float dg = s_gamma[j] * s_rgamma[an] * gacc[tc / kWaves][q];
+          if (mr < NT)
+            ab[blk(j, an)] = dg;
+          else if (an < j)
+            lk[s_off[j] + s_depth[an] - 1] = s_be[j] * dg;
+        }
+      }
+  }
+  __syncthreads();
+
+  if (w == kSetup) {
+    // ---- T = (I + Lk)^-1, row j along P(j), deepest ancestor first:
+    //      T_jj = 1,  T_ja = - sum_{e in P(j), a < e} T_je Lk_ea
+    if (l < n) {
+      const int j = l;
+      const uint64_t m = s_anc[j];
+      tb[blk(j, j)] = 1.f;
+      uint64_t rest = m & ~(1ull << j);
+      while (rest) {
+        const int an = 63 - __builtin_clzll(rest);
+        rest &= ~(1ull << an);
+        const int ta = s_depth[an] - 1;
+        uint64_t below = m & ~((2ull << an) - 1ull);
+        float sum = 0.f;
+        while (below) {
+          const int e = __builtin_ctzll(below);
+          below &= below - 1ull;
+          sum = __builtin_fmaf(-tb[blk(j, e)], lk[s_off[e] + ta], sum);
+        }
+        tb[blk(j, an)] = sum;
+      }
+    }
+    // factor records independent of the V-tile: k (from the staged rows), alpha, parent
+    if (tile == 0) {
+      bf16 *fk = static_cast<bf16 *>(a.fk);
+      for (int c = l; c < n * CH; c += kWave) {
+        const int j = c / CH, part = c % CH;
+        *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * 8) = xs[xchunk<CH>(NP + j, part)];
+      }
+      if (l < n) {
+        a.falpha[(nbase + l) * H + h] = al;
+        if (h == 0) a.fparent[nbase + l] = p;
+      }
+    }
+  }
+
+  // ---- column waves, K-step by K-step as the tile lands: delayed state
+  //      update, write-back of the committed rows, hi/lo split, and
+  //      P = [Q; K] H0 (accumulator layout: lane (lg, lc) holds rows
+  //      4 lg .. 4 lg + 3 of each 16-row tile, column lc)
+  f32x4 pacc[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) pacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 rreg[NT];
+  if (cols_live) {
+    const int ps = plen < kPMax ? plen : kPMax;
+    const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
+    const int pn = a.has_pending ? a.pend.n : 1;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (a.has_pending) {
+        for (int s = 0; s < ps; ++s) {
+          const float al = s_palpha[s];
+          const float uv = s_pu[s * kTileCols + ucol];
+          const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(s_pk + s * DK + ks * 32 + 8 * lg);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, static_cast<float>(kv[e]), uv);
+        }
+        // paths longer than the LDS stage read their records directly
+        for (int s = kPMax; s < plen; ++s) {
+          const int node = a.pend.path[(size_t)b * pn + s];
+          const size_t r = ((size_t)b * pn + node) * H + h;
+          const float al = a.pend.alpha[r];
+          const float uv = a.pend.u[r * dv + col];
+          float kr[8];
+          load_f32<8>(pkg + r * DK + ks * 32 + 8 * lg, kr);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, kr[e], uv);
+        }
+#pragma unroll
+        for (int e = 0; e < 8; ++e) buf_store_f32<kPolicyStream>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
+      }
+      bf16x8 bhi, blo;
+      split8(hf[ks], bhi, blo);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
+        pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pacc[mt], 0, 0, 0);
+        pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pacc[mt], 0, 0, 0);
+      }
+    }
+    // R = beta (v - gamma P_k) in the accumulator layout
+#pragma unroll
+    for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int j = mt * 16 + 4 * lg + q;
+        rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float((uint32_t)vraw[mt][q] << 16) - s_gamma[j] * pacc[NT + mt][q]) : 0.f;
+      }
+  }
+  __syncthreads();  // T complete
+  if (!cols_live) return;
+
+  // ---- U = T R, then O = Gamma P_q + Attn U, on the matrix cores; A
+  //      fragments are rows j = 16 mt + lc, columns 16 ks + 4 lg .. + 3
+  s16x4 rhi[NT], rlo[NT];
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
+  f32x4 uacc[NT];
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt) {
+    uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks <= mt; ++ks) {
+      const f32x4 tv = *reinterpret_cast<const f32x4 *>(tb + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
+      s16x4 th, tlo;
+      split4(tv, th, tlo);
+      uacc[mt] = mfma16_split(th, tlo, rhi[ks], rlo[ks], uacc[mt]);
+    }
+  }
+  s16x4 uhi[NT], ulo[NT];
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt) split4(uacc[mt], uhi[mt], ulo[mt]);
+  // outputs and corrected values of node j at ((b n + j) H + h) dv + col;
+  // rows past the last node fall outside the descriptors (the whole offset
+  // is carried per lane, where the range check applies) and are dropped
+  const uint32_t obytes = ((uint32_t)(n - 1) * nstride + dv) * 4;
+  const rsrc_t orr = make_rsrc(a.out + (nbase * H + h) * dv, obytes);
+  const rsrc_t urr = make_rsrc(a.fu + (nbase * H + h) * dv, obytes);
+  const uint32_t ov = (4 * lg * nstride + col) * 4;
+#pragma unroll
+  for (int mt = 0; mt < NT; ++mt) {
+    f32x4 oacc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks <= mt; ++ks) {
+      const f32x4 av = *reinterpret_cast<const f32x4 *>(ab + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
+      s16x4 ah, alo;
+      split4(av, ah, alo);
+      oacc = mfma16_split(ah, alo, uhi[ks], ulo[ks], oacc);
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int j = mt * 16 + 4 * lg + q;
+      const uint32_t vo = ov + (uint32_t)(mt * 16 + q) * nstride * 4;
+      buf_store_f32<kPolicyStream>(uacc[mt][q], urr, vo, 0);
+      buf_store_f32<kPolicyStream>(__builtin_fmaf(s_gamma[j], pacc[mt][q], oacc[q]), orr, vo, 0);
+    }
+  }
+}
+
+constexpr size_t kMaxLds = 160 * 1024;
+constexpr size_t kDefaultLds = 64 * 1024;
+
+template <int DK, int NP>
+hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
+  const size_t lds = Layout<DK, NP>::kBytes;
+  if (lds > kMaxLds) return hipErrorInvalidConfiguration;
+  auto kern = verify_tile_kernel<DK, NP>;
+  if (lds > kDefaultLds) {
+    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  const int ntiles = (a.dv + kTileCols - 1) / kTileCols;
+  const dim3 grid((unsigned)((size_t)a.B * a.H * ntiles));
+  hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int DK>
+hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
+  if (a.n <= 16) return launch_np<DK, 16>(a, s);
+  if (a.n <= 32) return launch_np<DK, 32>(a, s);
+  return launch_np<DK, 64>(a, s);
+}
+
+}  // namespace
+
+bool parallel_supported(int dk, int dv, int n, int dtype) {
+  // The hi/lo split contraction relies on q and k being exact in bf16.
+  return dtype == SLA_DTYPE_BF16 && (dk == 64 || dk == 128 || dk == 256) && dv % 16 == 0 && n >= 1 &&
+         n <= SLA_MAX_NODES;
+}
+
+hipError_t launch_verify_parallel(const VerifyArgs &a, int dtype, hipStream_t s) {
+  if (dtype != SLA_DTYPE_BF16) return hipErrorInvalidConfiguration;
+  switch (a.dk) {
+    case 64: return launch_dk<64>(a, s);
+    case 128: return launch_dk<128>(a, s);
+    case 256: return launch_dk<256>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace sla
