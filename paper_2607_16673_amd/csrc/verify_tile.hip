@@ -26,14 +26,17 @@
 //              v_mfma_f32_16x16x16bf16_1k (whose B fragment is exactly the
 //              accumulator layout holding R, then U), and the outputs.
 //   wave 4     owns no state.  It takes every read that depends on another
-//              read: parent row and gates -> topology, decays and compact-list
-//              offsets; pending path -> validation and the factor records it
-//              names; and it stages [Q; K] with direct global->LDS loads.
-//              After the Grams it solves the per-node rows of T.
+//              read or that everything else waits for: parent row and gates
+//              -> topology, decays and compact-list offsets; the pending path
+//              with the previous round's parent row and gates -> validation;
+//              [Q; K] by direct global->LDS loads; then, while the column
+//              waves compute the Grams, the factor records the path names
+//              (also straight into LDS).  After the Grams it solves the
+//              per-node rows of T.
 // The tree-masked Grams ([Q; K] K^T tiles that hold ancestor pairs, exact
-// bf16 products) are spread over all five waves; they and T are done while
-// the state tile is still in flight.  Strided global accesses go through
-// buffer descriptors (one VGPR offset per lane).
+// bf16 products) run on the column waves; they and T are done while the
+// state tile is still in flight.  Strided global accesses go through buffer
+// descriptors (one VGPR offset per lane).
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -83,6 +86,15 @@ __device__ __forceinline__ void load_lds16(const void *g, void *lds_wave_base) {
   __builtin_amdgcn_global_load_lds(g, (lds_void *)(lds_wave_base), 16, 0, 0);
 }
 
+// Each lane's 4 bytes land at lds_wave_base + 4 * lane.
+__device__ __forceinline__ void load_lds4(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)(lds_wave_base), 4, 0, 0);
+}
+
+// s_waitcnt immediate that waits until at most `n` vector memory operations
+// of this wave are outstanding (export and LDS counters unconstrained).
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
 // element (row j, column a), a <= j, of a lower-triangular 16x16-blocked matrix
 __device__ __forceinline__ int blk(int j, int a) {
   const int bj = j >> 4;
@@ -124,7 +136,7 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
   using L = Layout<DK, NP>;
   constexpr int KS = L::KS, NT = L::NT, MT = L::MT, CH = L::CH;
   constexpr int NGT = NT * (NT + 1);                 // Gram tiles (both halves)
-  constexpr int GT = (NGT + kWaves - 1) / kWaves;    // Gram tiles per wave
+  constexpr int GT = (NGT + kColWaves - 1) / kColWaves;  // Gram tiles per column wave
 
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint4 *xs = reinterpret_cast<uint4 *>(lds);                              // [Q; K]
@@ -187,7 +199,9 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
   // ---- setup wave: everything that depends on another read
   int p = -1;      // setup wave, lane j: parent of node j
   float al = 1.f;  // setup wave, lane j: alpha_j
+  int nodec = 0;   // setup wave, lane t: node of pending step t (clamped into the store)
   if (w == kSetup) {
+    for (int c = l; c < (L::kT + L::kAt) / 16; c += kWave) reinterpret_cast<uint4 *>(tb)[c] = make_uint4(0, 0, 0, 0);
     const bf16 *qg = static_cast<const bf16 *>(a.q);
     const bf16 *kg = static_cast<const bf16 *>(a.k);
     const bool live = l < n;
@@ -195,13 +209,17 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
     p = live ? a.parent[nbase + l] : -1;
     al = live ? a.alpha[s] : 1.f;
     const float be = live ? a.beta[s] : 0.f;
-    int plen = 0, node = -1, prev = -1;
+    // pending accepted path, with the previous round's parent row and gates
+    // read whole, so that validating the path waits on no further read
+    int plen = 0, node = -1, prow_parent = -2;
+    float prow_alpha = 0.f;
     const int pn = a.has_pending ? a.pend.n : 1;
+    const size_t prow = (size_t)b * pn;
     if (a.has_pending) {
-      const int32_t *prow = a.pend.path + (size_t)b * pn;
       plen = a.pend.len[b];
-      node = l < pn ? prow[l] : -1;
-      prev = (l >= 1 && l - 1 < pn) ? prow[l - 1] : -1;
+      node = l < pn ? a.pend.path[prow + l] : -1;
+      prow_parent = l < pn ? a.pend.parent[prow + l] : -2;
+      prow_alpha = l < pn ? a.pend.alpha[(prow + l) * H + h] : 0.f;
     }
     // [Q; K] straight into LDS (rows 0..NP-1: q_j, NP..2NP-1: k_j; padding
     // rows repeat node 0 and are never used)
@@ -212,7 +230,6 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
       const int j = row % NP;
       load_lds16((row < NP ? qg : kg) + ((nbase + (j < n ? j : 0)) * H + h) * DK + c * 8, xs + i * kWave);
     }
-    for (int c = l; c < (L::kT + L::kAt) / 16; c += kWave) reinterpret_cast<uint4 *>(tb)[c] = make_uint4(0, 0, 0, 0);
 
     // topology, decays and compact-list offsets; lane j owns node j
     bool bad = live && (p < -1 || p >= l);
@@ -249,48 +266,57 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
         s_be[l] = be;
       }
     }
-    // pending accepted path: validate (one dependent read) and stage records
+    // the path: step t is node path[t], whose parent must be path[t - 1]
+    // (-1 for t = 0)
+    const bool inrange = node >= 0 && node < pn;
+    nodec = inrange ? node : 0;
     if (err == SLA_OK && a.has_pending) {
+      int prev = __shfl_up(node, 1);
+      if (l == 0) prev = -1;
+      const int ppar = __shfl(prow_parent, nodec);
+      const float pal = __shfl(prow_alpha, nodec);
       const bool step = l < plen;
-      const bool inrange = node >= 0 && node < pn;
-      const size_t srec = ((size_t)b * pn + (inrange ? node : 0)) * H + h;
-      const int ppar = (step && inrange) ? a.pend.parent[(size_t)b * pn + node] : -2;
-      const float pal = (step && inrange) ? a.pend.alpha[srec] : 0.f;
       const bool pbad = (plen < 0 || plen > pn) || (step && (!inrange || ppar != prev));
       err = wave_any(pbad) ? SLA_ERR_PATH : SLA_OK;
-      if (err == SLA_OK) {
-        const int ps = plen < kPMax ? plen : kPMax;
-        if (l < kPMax) s_palpha[l] = l < ps ? pal : 0.f;
-        const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
-#pragma unroll
-        for (int i = 0; i < kPMax * CH / kWave; ++i) {
-          const int P = i * kWave + l;
-          const int t = P / CH, c = P % CH;
-          const int nt = __shfl(node, t);
-          load_lds16(pkg + (t < ps ? (((size_t)b * pn + nt) * H + h) * DK + c * 8 : 0), s_pk + i * kWave * 8);
-        }
-        const int cg = tile * kTileCols + l;
-#pragma unroll
-        for (int t = 0; t < kPMax; ++t) {
-          const int nt = __builtin_amdgcn_readlane(node, t);
-          s_pu[t * kTileCols + l] =
-              (t < ps && cg < dv) ? a.pend.u[(((size_t)b * pn + nt) * H + h) * dv + cg] : 0.f;
-        }
-      }
+      if (l < kPMax) s_palpha[l] = l < plen ? pal : 0.f;
     }
     if (l == 0) {
       s_misc[0] = err;
       s_misc[1] = plen;
     }
     if (tile == 0 && h == 0 && l == 0 && a.status) a.status[b] = err;
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's direct LDS loads have landed
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // [Q; K] has landed
   }
   __syncthreads();
   const int err = s_misc[0];
   if (err != SLA_OK) return;
   const int plen = s_misc[1];
 
-  // ---- tree-masked Grams over all waves: tile (mr, na) of [Q; K] K^T holds
+  // ---- setup wave: records of the first kPMax path nodes, gathered straight
+  //      into LDS while the column waves compute the Grams; they are the
+  //      wave's only LDS writes until the second barrier, which waits for them
+  if (w == kSetup && a.has_pending) {
+    const int pn = a.pend.n;
+    const size_t prow = (size_t)b * pn;
+    const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
+    constexpr int KI = kPMax * CH / kWave;
+    int nt[KI];  // node of the step whose key chunk this lane gathers
+#pragma unroll
+    for (int i = 0; i < KI; ++i) nt[i] = __shfl(nodec, (i * kWave + l) / CH);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < KI; ++i)
+      load_lds16(pkg + ((prow + nt[i]) * H + h) * DK + ((i * kWave + l) % CH) * 8, s_pk + i * kWave * 8);
+    const int cg = tile * kTileCols + l;
+    const int cc = cg < dv ? cg : dv - 1;
+#pragma unroll
+    for (int t = 0; t < kPMax; ++t) {
+      const int ntt = __builtin_amdgcn_readlane(nodec, t);
+      load_lds4(a.pend.u + ((prow + ntt) * H + h) * dv + cc, s_pu + t * kTileCols);
+    }
+  }
+
+  // ---- tree-masked Grams over the column waves: tile (mr, na) of [Q; K] K^T holds
   //      rows of node tile mr % NT against ancestor candidates of node tile
   //      na <= mr % NT; ancestor entries go to Attn blocks and Lk lists
   {
@@ -300,7 +326,7 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
     for (int mr = 0; mr < MT; ++mr)
 #pragma unroll
       for (int na = 0; na <= mr % NT; ++na, ++tc) {
-        if (tc % kWaves != w || (mr % NT) * 16 >= n) continue;
+        if (tc % kColWaves != w || (mr % NT) * 16 >= n) continue;
         f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -308,21 +334,21 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
           const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
           g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, g, 0, 0, 0);
         }
-        gacc[tc / kWaves] = g;
+        gacc[tc / kColWaves] = g;
       }
     tc = 0;
 #pragma unroll
     for (int mr = 0; mr < MT; ++mr)
 #pragma unroll
       for (int na = 0; na <= mr % NT; ++na, ++tc) {
-        if (tc % kWaves != w || (mr % NT) * 16 >= n) continue;
+        if (tc % kColWaves != w || (mr % NT) * 16 >= n) continue;
         const int an = na * 16 + lc;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int j = (mr % NT) * 16 + 4 * lg + q;
           if (j >= n || an > j) continue;
           if (!((s_anc[j] >> an) & 1ull)) continue;
-          const float dg = s_gamma[j] * s_rgamma[an] * gacc[tc / kWaves][q];
+          const float dg = s_gamma[j] * s_rgamma[an] * gacc[tc / kColWaves][q];
           if (mr < NT)
             ab[blk(j, an)] = dg;
           else if (an < j)
@@ -330,6 +356,7 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
         }
       }
   }
+  if (w == kSetup) __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // the gathered records have landed
   __syncthreads();
 
   if (w == kSetup) {
@@ -380,30 +407,42 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
     const int ps = plen < kPMax ? plen : kPMax;
     const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
     const int pn = a.has_pending ? a.pend.n : 1;
+    if (a.has_pending) {
+      // the whole tile has normally landed by now: step-major, one LDS round
+      // trip per step
+      for (int s = 0; s < ps; ++s) {
+        const float al = s_palpha[s];
+        const float uv = s_pu[s * kTileCols + ucol];
+        bf16x8 kv[KS];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      if (a.has_pending) {
-        for (int s = 0; s < ps; ++s) {
-          const float al = s_palpha[s];
-          const float uv = s_pu[s * kTileCols + ucol];
-          const bf16x8 kv = *reinterpret_cast<const bf16x8 *>(s_pk + s * DK + ks * 32 + 8 * lg);
+        for (int ks = 0; ks < KS; ++ks) kv[ks] = *reinterpret_cast<const bf16x8 *>(s_pk + s * DK + ks * 32 + 8 * lg);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, static_cast<float>(kv[e]), uv);
-        }
-        // paths longer than the LDS stage read their records directly
-        for (int s = kPMax; s < plen; ++s) {
-          const int node = a.pend.path[(size_t)b * pn + s];
-          const size_t r = ((size_t)b * pn + node) * H + h;
-          const float al = a.pend.alpha[r];
-          const float uv = a.pend.u[r * dv + col];
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, static_cast<float>(kv[ks][e]), uv);
+      }
+      // paths longer than the LDS stage read their records directly
+      for (int s = kPMax; s < plen; ++s) {
+        const int node = a.pend.path[(size_t)b * pn + s];
+        const size_t r = ((size_t)b * pn + node) * H + h;
+        const float al = a.pend.alpha[r];
+        const float uv = a.pend.u[r * dv + col];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
           float kr[8];
           load_f32<8>(pkg + r * DK + ks * 32 + 8 * lg, kr);
 #pragma unroll
           for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, kr[e], uv);
         }
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int e = 0; e < 8; ++e) buf_store_f32<kPolicyStream>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
-      }
+    }
+    // hi/lo split and P = [Q; K] H0, K-step by K-step as the tile lands
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
       bf16x8 bhi, blo;
       split8(hf[ks], bhi, blo);
 #pragma unroll
@@ -419,7 +458,9 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int j = mt * 16 + 4 * lg + q;
-        rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float((uint32_t)vraw[mt][q] << 16) - s_gamma[j] * pacc[NT + mt][q]) : 0.f;
+        uint32_t vb = vraw[mt][q];
+        __asm__("" : "+v"(vb));  // keeps the widening here, not next to the load
+        rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float(vb << 16) - s_gamma[j] * pacc[NT + mt][q]) : 0.f;
       }
   }
   __syncthreads();  // T complete
