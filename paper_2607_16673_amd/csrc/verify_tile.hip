@@ -131,12 +131,19 @@ __device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x
   return mfma16(al, bh, acc);
 }
 
+// Waves per SIMD the register allocation is held to: 6 (80 VGPRs) where the
+// tile state, accumulators and LDS allow a fourth resident workgroup per CU,
+// else whatever the allocation needs.
 template <int DK, int NP>
-__global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
+constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
+
+template <int DK, int NP>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP>)))
+void verify_tile_kernel(VerifyArgs a) {
   using L = Layout<DK, NP>;
   constexpr int KS = L::KS, NT = L::NT, MT = L::MT, CH = L::CH;
-  constexpr int NGT = NT * (NT + 1);                 // Gram tiles (both halves)
-  constexpr int GT = (NGT + kColWaves - 1) / kColWaves;  // Gram tiles per column wave
+  constexpr int NGT = NT * (NT + 1);                        // Gram tiles (both halves)
+  constexpr int GT = (NGT + kColWaves - 1) / kColWaves;     // Gram tiles per column wave
 
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
   uint4 *xs = reinterpret_cast<uint4 *>(lds);                              // [Q; K]
@@ -342,17 +349,34 @@ __global__ __launch_bounds__(kThreads) void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
       for (int na = 0; na <= mr % NT; ++na, ++tc) {
         if (tc % kColWaves != w || (mr % NT) * 16 >= n) continue;
+        // every LDS read of the tile's metadata is issued before its first
+        // write, so they share one round trip
         const int an = na * 16 + lc;
+        const int jb = (mr % NT) * 16 + 4 * lg;
+        uint32_t anc[4];  // the half of row j's ancestor mask that holds column an
+        float gj[4], bj[4];
+        int oj[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int j = (mr % NT) * 16 + 4 * lg + q;
-          if (j >= n || an > j) continue;
-          if (!((s_anc[j] >> an) & 1ull)) continue;
-          const float dg = s_gamma[j] * s_rgamma[an] * gacc[tc / kColWaves][q];
+          anc[q] = reinterpret_cast<const uint32_t *>(s_anc)[2 * (jb + q) + (na >> 1)];
+          gj[q] = s_gamma[jb + q];
+          if (mr >= NT) {
+            bj[q] = s_be[jb + q];
+            oj[q] = s_off[jb + q];
+          }
+        }
+        const float ra = s_rgamma[an];
+        const int da = mr >= NT ? s_depth[an] : 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = jb + q;
+          // rows past the last node hold stale LDS words: masked by j < n
+          if (j >= n || an > j || (mr >= NT && an == j) || !((anc[q] >> (an & 31)) & 1u)) continue;
+          const float dg = gj[q] * ra * gacc[tc / kColWaves][q];
           if (mr < NT)
             ab[blk(j, an)] = dg;
-          else if (an < j)
-            lk[s_off[j] + s_depth[an] - 1] = s_be[j] * dg;
+          else
+            lk[oj[q] + da - 1] = bj[q] * dg;
         }
       }
   }
