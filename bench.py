@@ -238,7 +238,9 @@ def main():
         with open(args.traffic_json) as f:
             tj = json.load(f)
         key = "%s/%s/%s" % (cfg.name, args.route, "separate" if args.separate else "fused")
-        if key in tj:
+        # counters taken on other library sources no longer describe this kernel
+        from paper_2607_16673_amd.traffic import source_digest
+        if key in tj and tj[key].get("source_sha256") == source_digest():
             traffic = tj[key].get("bytes_per_launch")
             kernel = tj[key].get("kernel")
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",

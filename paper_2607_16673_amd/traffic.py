@@ -1,0 +1,150 @@
+"""Measured HBM traffic of the verify kernel from rocprofv3 counters.
+
+Two steps, each run under its own `rocprofv3 --pmc <counter>` pass (one
+pass for FETCH_SIZE, one for WRITE_SIZE; the counters cannot share a pass):
+
+  copy      a plain device copy of a known size (reads N bytes, writes N
+            bytes), the calibration: the counters' KiB per dispatch are
+            scaled so that this copy reads and writes exactly N bytes;
+  summarize reads the counter CSVs of the copy passes and of the bench
+            passes and writes the calibrated HBM bytes per verify launch to
+            profiles/traffic.json, which bench.py reports as
+            roofline.traffic.
+
+Example (the full commands are recorded next to the numbers in profiles/):
+
+  rocprofv3 --pmc FETCH_SIZE -d OUT/copy_fetch --output-format csv -- \\
+      python3 -m paper_2607_16673_amd.traffic copy
+  rocprofv3 --pmc FETCH_SIZE -d OUT/bench_fetch --output-format csv -- \\
+      python3 bench.py --no-graph --steps 2 --warmup 1 --no-cpu-baseline
+  (the same two with WRITE_SIZE)
+  python3 -m paper_2607_16673_amd.traffic summarize --out-dir OUT \\
+      --workload batched_tree_serving
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import sys
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+COPY_MIB = 512
+KERNEL_TAG = "verify_tile_kernel"
+COPY_TAG = "mul"  # the elementwise multiply of run_copy (not the fill before it)
+
+
+def source_digest() -> str:
+    """sha256 over the library sources: counters taken on other sources are stale."""
+    h = hashlib.sha256()
+    files = sorted(glob.glob(os.path.join(HERE, "csrc", "*"))) + [os.path.join(ROOT, "include", "sla.h")]
+    for fn in files:
+        with open(fn, "rb") as f:
+            h.update(os.path.basename(fn).encode() + b"\0" + f.read())
+    return h.hexdigest()
+
+
+def run_copy(mib: int = COPY_MIB) -> None:
+    """Elementwise device copy of `mib` MiB (fp32), five dispatches."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    a = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        torch.mul(a, 1.0, out=b)  # one elementwise kernel: reads a, writes b
+    torch.cuda.synchronize()
+    print("copy: %d MiB x 5 dispatches" % mib, flush=True)
+
+
+def _rows(dirname: str, counter: str):
+    files = glob.glob(os.path.join(dirname, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise FileNotFoundError("no counter_collection.csv under %s" % dirname)
+    out = []
+    for fn in files:
+        with open(fn, newline="") as f:
+            for r in csv.DictReader(f):
+                if r.get("Counter_Name") == counter:
+                    out.append(r)
+    out.sort(key=lambda r: int(r.get("Dispatch_Id") or r.get("Correlation_Id") or 0))
+    return out
+
+
+def _per_dispatch_kib(rows, tag, skip=0):
+    # a counter may be reported per XCD / per instance: sum per dispatch
+    acc = {}
+    order = []
+    for r in rows:
+        if tag.lower() not in r.get("Kernel_Name", "").lower():
+            continue
+        d = r.get("Dispatch_Id") or r.get("Correlation_Id")
+        if d not in acc:
+            acc[d] = 0.0
+            order.append(d)
+        acc[d] += float(r["Counter_Value"])
+    vals = [acc[d] for d in order][skip:]
+    if not vals:
+        raise ValueError("no dispatch of a kernel matching %r" % tag)
+    return sum(vals) / len(vals), len(vals)
+
+
+def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, json_path: str) -> dict:
+    copy_bytes = COPY_MIB * (1 << 20)  # per copy dispatch, read and written
+    cf, _ = _per_dispatch_kib(_rows(os.path.join(out_dir, "copy_fetch"), "FETCH_SIZE"), COPY_TAG, 0)
+    cw, _ = _per_dispatch_kib(_rows(os.path.join(out_dir, "copy_write"), "WRITE_SIZE"), COPY_TAG, 0)
+    scale_f = copy_bytes / (cf * 1024.0)
+    scale_w = copy_bytes / (cw * 1024.0)
+    bf, nf = _per_dispatch_kib(_rows(os.path.join(out_dir, "bench_fetch"), "FETCH_SIZE"), KERNEL_TAG, skip)
+    bw, nw = _per_dispatch_kib(_rows(os.path.join(out_dir, "bench_write"), "WRITE_SIZE"), KERNEL_TAG, skip)
+    fetch = bf * 1024.0 * scale_f
+    write = bw * 1024.0 * scale_w
+    key = "%s/%s/%s" % (workload, route, mode)
+    entry = {
+        "kernel": KERNEL_TAG,
+        "bytes_per_launch": int(round(fetch + write)),
+        "fetch_bytes_per_launch": int(round(fetch)),
+        "write_bytes_per_launch": int(round(write)),
+        "fetch_kib_raw": round(bf, 1), "write_kib_raw": round(bw, 1),
+        "copy_scale_fetch": round(scale_f, 4), "copy_scale_write": round(scale_w, 4),
+        "dispatches": [nf, nw],
+        "source_sha256": source_digest(),
+    }
+    data = {}
+    if os.path.exists(json_path):
+        with open(json_path) as f:
+            data = json.load(f)
+    data[key] = entry
+    with open(json_path, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+        f.write("\n")
+    return {key: entry}
+
+
+def main(argv=None) -> None:
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    c = sub.add_parser("copy")
+    c.add_argument("--mib", type=int, default=COPY_MIB)
+    s = sub.add_parser("summarize")
+    s.add_argument("--out-dir", required=True)
+    s.add_argument("--workload", required=True)
+    s.add_argument("--route", default="auto")
+    s.add_argument("--mode", default="fused")
+    s.add_argument("--skip", type=int, default=0,
+                   help="leading verify dispatches to ignore (the first step has no pending path)")
+    s.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    a = ap.parse_args(argv)
+    if a.cmd == "copy":
+        run_copy(a.mib)
+    else:
+        print(json.dumps(summarize(a.out_dir, a.workload, a.route, a.mode, a.skip, a.json), indent=1))
+
+
+if __name__ == "__main__":
+    sys.exit(main())
