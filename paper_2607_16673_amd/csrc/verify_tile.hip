@@ -16,10 +16,14 @@
 //
 // One workgroup = one (batch b, head h, 64-column V-tile), five wavefronts:
 //   waves 0-3  own 16 state columns each.  They issue the state tile reads
-//              (non-temporal, in the B-fragment order of
-//              v_mfma_f32_16x16x32_bf16: 8 consecutive rows of one column per
-//              32-row K-step) and the value reads first thing, and consume the
-//              tile K-step by K-step as it lands: pending path applied,
+//              (in the B-fragment order of v_mfma_f32_16x16x32_bf16: 8
+//              consecutive rows of one column per 32-row K-step) and the
+//              value reads first thing.  The reads keep the default cache
+//              policy: a wave covers only half of each 128-byte line, and
+//              with a streaming hint the L2 lets the line go before the
+//              neighbouring wave asks for the other half (measured: about
+//              15% more HBM reads).  The tile is consumed
+//              K-step by K-step as it lands: pending path applied,
 //              committed rows written back, fp32 split into bf16 hi + lo,
 //              P = [Q; K] H0 accumulated on the matrix cores.  Then
 //              R = beta (v - gamma P_k), U = T R and O = Gamma P_q + Attn U on
@@ -48,17 +52,13 @@ typedef __attribute__((ext_vector_type(4))) short s16x4;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kColWaves = 4;
-constexpr int kSetup = kColWaves;                // wave index of the setup wave
-constexpr int kWaves = kColWaves + 1;
-constexpr int kThreads = kWaves * kWave;         // 320
-constexpr int kWaveCols = 16;
-constexpr int kTileCols = kColWaves * kWaveCols;  // 64 state columns per workgroup
+constexpr int kWaveCols = 16;                    // state columns per column wave
 constexpr int kPMax = 8;                          // pending steps staged in LDS
 constexpr int kBP = 20;                           // fp32 row pitch of a 16x16 block
 
-template <int DK, int NP>
+template <int DK, int NP, int CW, int TPW>
 struct Layout {
+  static constexpr int kTileCols = CW * kWaveCols;
   static constexpr int NT = NP / 16, KS = DK / 32, CH = DK / 8, MT = 2 * NT;
   static constexpr int NB = NT * (NT + 1) / 2;      // lower-triangular 16x16 blocks
   static constexpr int kList = NP * (NP + 1) / 2;   // compact Lk capacity (floats)
@@ -68,7 +68,7 @@ struct Layout {
   static constexpr int kAt = NB * kBlk;             // Attn blocks
   static constexpr int kLk = kList * 4;
   static constexpr int kPk = kPMax * DK * 2;        // pending keys (bf16)
-  static constexpr int kPu = kPMax * kTileCols * 4; // pending corrected values of this tile
+  static constexpr int kPu = (TPW > 1 ? 2 : 1) * kPMax * kTileCols * 4;  // pending corrected values, per tile
   static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 4 + 16;
   static constexpr int kBytes = kX + kT + kAt + kLk + kPk + kPu + kTopo;
 };
@@ -134,13 +134,16 @@ __device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x
 // Waves per SIMD the register allocation is held to: 6 (80 VGPRs) where the
 // tile state, accumulators and LDS allow a fourth resident workgroup per CU,
 // else whatever the allocation needs.
-template <int DK, int NP>
-constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
+template <int DK, int NP, int TPW>
+constexpr int kMinWaves = (DK <= 128 && NP <= 16 && TPW == 1) ? 6 : 1;
 
-template <int DK, int NP>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP>)))
+template <int DK, int NP, int CW, int TPW>
+__global__ __launch_bounds__((CW + 1) * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
 void verify_tile_kernel(VerifyArgs a) {
-  using L = Layout<DK, NP>;
+  using L = Layout<DK, NP, CW, TPW>;
+  constexpr int kColWaves = CW;                 // waves 0 .. CW-1 own state columns
+  constexpr int kSetup = CW;                    // the setup wave
+  constexpr int kTileCols = L::kTileCols;       // state columns per workgroup
   constexpr int KS = L::KS, NT = L::NT, MT = L::MT, CH = L::CH;
   constexpr int NGT = NT * (NT + 1);                        // Gram tiles (both halves)
   constexpr int GT = (NGT + kColWaves - 1) / kColWaves;     // Gram tiles per column wave
@@ -168,39 +171,49 @@ void verify_tile_kernel(VerifyArgs a) {
   const int lc = l & 15;  // column within a wave's 16 / row within a 16-row tile
   const int lg = l >> 4;  // row group
   const int H = a.H, dv = a.dv, n = a.n;
+  // this workgroup: unit (b, h), V-tiles t0 .. t0 + cnt - 1
   const int ntiles = (dv + kTileCols - 1) / kTileCols;
+  const int ngroups = (ntiles + TPW - 1) / TPW;
   int wid = blockIdx.x;
-  const int tile = wid % ntiles;
-  wid /= ntiles;
+  const int t0 = (wid % ngroups) * TPW;
+  wid /= ngroups;
+  const int cnt = TPW;  // TPW divides the tile count (the launcher checks)
   const int h = wid % H;
   const int b = wid / H;
-  const int ucol = w * kWaveCols + lc;  // column within the tile
-  const int col = tile * kTileCols + ucol;
-  const bool cols_live = w < kColWaves && tile * kTileCols + w * kWaveCols < dv;  // wave-uniform
+  const int ucol = w * kWaveCols + lc;  // column within a tile
   const size_t unit = (size_t)b * H + h;
   const size_t nbase = (size_t)b * n;
   const rsrc_t sr = make_rsrc(a.state + unit * DK * dv, (uint32_t)DK * dv * 4);
-  const uint32_t sv = (uint32_t)(8 * lg * dv + col) * 4;
   const uint32_t nstride = (uint32_t)H * dv;  // elements between consecutive nodes of a unit
-
-  // ---- column waves: the state tile and the values, issued first
-  float hf[KS][8];
-  uint32_t vraw[NT][4];  // bf16 bit patterns, widened where they are used
-  if (cols_live) {
+  const rsrc_t vr = make_rsrc(static_cast<const bf16 *>(a.v) + (nbase * H + h) * dv,
+                              ((uint32_t)(n - 1) * nstride + dv) * 2);
+  // wave-uniform: this wave owns columns of tile t
+  auto live = [&](int t) { return w < kColWaves && t * kTileCols + w * kWaveCols < dv; };
+  // state rows 8 lg + e + 32 ks of column t * kTileCols + ucol, in B-fragment order
+  auto load_state = [&](int t, float (&hf)[KS][8]) {
+    const uint32_t sv = (uint32_t)(8 * lg * dv + t * kTileCols + ucol) * 4;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-      for (int e = 0; e < 8; ++e) hf[ks][e] = buf_load_f32<kPolicyStream>(sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
-    // node j = 16 mt + 4 lg + q; rows past the last node fall outside the
-    // descriptor and read zero
-    const rsrc_t vr = make_rsrc(static_cast<const bf16 *>(a.v) + (nbase * H + h) * dv,
-                                ((uint32_t)(n - 1) * nstride + dv) * 2);
-    const uint32_t vv = (4 * lg * nstride + col) * 2;
+      for (int e = 0; e < 8; ++e) hf[ks][e] = buf_load_f32<kPolicyDefault>(sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
+  };
+  // values of node j = 16 mt + 4 lg + q; rows past the last node fall
+  // outside the descriptor and read zero
+  auto load_values = [&](int t, uint32_t (&vraw)[NT][4]) {
+    const uint32_t vv = (4 * lg * nstride + t * kTileCols + ucol) * 2;
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         vraw[mt][q] = __builtin_amdgcn_raw_buffer_load_b16(vr, vv + (uint32_t)(mt * 16 + q) * nstride * 2, 0, kPolicyDefault);
+  };
+
+  // ---- column waves: the first tile's state and values, issued first
+  float hfa[KS][8], hfb[KS][8];  // hfb: the next tile's state (prefetching form only)
+  uint32_t vraw[NT][4];  // bf16 bit patterns, widened where they are used
+  if (live(t0)) {
+    load_state(t0, hfa);
+    load_values(t0, vraw);
   }
 
   // ---- setup wave: everything that depends on another read
@@ -291,7 +304,7 @@ void verify_tile_kernel(VerifyArgs a) {
       s_misc[0] = err;
       s_misc[1] = plen;
     }
-    if (tile == 0 && h == 0 && l == 0 && a.status) a.status[b] = err;
+    if (t0 == 0 && h == 0 && l == 0 && a.status) a.status[b] = err;
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // [Q; K] has landed
   }
   __syncthreads();
@@ -300,11 +313,23 @@ void verify_tile_kernel(VerifyArgs a) {
   const int plen = s_misc[1];
 
   // ---- setup wave: records of the first kPMax path nodes, gathered straight
-  //      into LDS while the column waves compute the Grams; they are the
-  //      wave's only LDS writes until the second barrier, which waits for them
+  //      into LDS while the column waves compute; a gather is the wave's
+  //      only LDS write until the next barrier, which waits for it
+  const size_t prow = (size_t)b * (a.has_pending ? a.pend.n : 1);
+  // corrected values of tile t (its columns) into stage buffer `buf`
+  auto gather_u = [&](int t, int buf) {
+#pragma unroll
+    for (int st = 0; st < kPMax; ++st) {
+      const int ntt = __builtin_amdgcn_readlane(nodec, st);
+#pragma unroll
+      for (int c0 = 0; c0 < kTileCols; c0 += kWave) {
+        const int cg = t * kTileCols + c0 + l;
+        load_lds4(a.pend.u + ((prow + ntt) * H + h) * dv + (cg < dv ? cg : dv - 1),
+                  s_pu + (buf * kPMax + st) * kTileCols + c0);
+      }
+    }
+  };
   if (w == kSetup && a.has_pending) {
-    const int pn = a.pend.n;
-    const size_t prow = (size_t)b * pn;
     const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
     constexpr int KI = kPMax * CH / kWave;
     int nt[KI];  // node of the step whose key chunk this lane gathers
@@ -314,13 +339,7 @@ void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
     for (int i = 0; i < KI; ++i)
       load_lds16(pkg + ((prow + nt[i]) * H + h) * DK + ((i * kWave + l) % CH) * 8, s_pk + i * kWave * 8);
-    const int cg = tile * kTileCols + l;
-    const int cc = cg < dv ? cg : dv - 1;
-#pragma unroll
-    for (int t = 0; t < kPMax; ++t) {
-      const int ntt = __builtin_amdgcn_readlane(nodec, t);
-      load_lds4(a.pend.u + ((prow + ntt) * H + h) * dv + cc, s_pu + t * kTileCols);
-    }
+    gather_u(t0, 0);
   }
 
   // ---- tree-masked Grams over the column waves: tile (mr, na) of [Q; K] K^T holds
@@ -406,7 +425,7 @@ void verify_tile_kernel(VerifyArgs a) {
       }
     }
     // factor records independent of the V-tile: k (from the staged rows), alpha, parent
-    if (tile == 0) {
+    if (t0 == 0) {
       bf16 *fk = static_cast<bf16 *>(a.fk);
       for (int c = l; c < n * CH; c += kWave) {
         const int j = c / CH, part = c % CH;
@@ -419,148 +438,189 @@ void verify_tile_kernel(VerifyArgs a) {
     }
   }
 
-  // ---- column waves, K-step by K-step as the tile lands: delayed state
-  //      update, write-back of the committed rows, hi/lo split, and
-  //      P = [Q; K] H0 (accumulator layout: lane (lg, lc) holds rows
-  //      4 lg .. 4 lg + 3 of each 16-row tile, column lc)
-  f32x4 pacc[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) pacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  f32x4 rreg[NT];
-  if (cols_live) {
-    const int ps = plen < kPMax ? plen : kPMax;
-    const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
-    const int pn = a.has_pending ? a.pend.n : 1;
-    if (a.has_pending) {
-      // the whole tile has normally landed by now: step-major, one LDS round
-      // trip per step
-      for (int s = 0; s < ps; ++s) {
-        const float al = s_palpha[s];
-        const float uv = s_pu[s * kTileCols + ucol];
-        bf16x8 kv[KS];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) kv[ks] = *reinterpret_cast<const bf16x8 *>(s_pk + s * DK + ks * 32 + 8 * lg);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, static_cast<float>(kv[ks][e]), uv);
-      }
-      // paths longer than the LDS stage read their records directly
-      for (int s = kPMax; s < plen; ++s) {
-        const int node = a.pend.path[(size_t)b * pn + s];
-        const size_t r = ((size_t)b * pn + node) * H + h;
-        const float al = a.pend.alpha[r];
-        const float uv = a.pend.u[r * dv + col];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          float kr[8];
-          load_f32<8>(pkg + r * DK + ks * 32 + 8 * lg, kr);
-#pragma unroll
-          for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, kr[e], uv);
-        }
-      }
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) buf_store_f32<kPolicyStream>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
-    }
-    // hi/lo split and P = [Q; K] H0, K-step by K-step as the tile lands
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      bf16x8 bhi, blo;
-      split8(hf[ks], bhi, blo);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
-        pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pacc[mt], 0, 0, 0);
-        pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pacc[mt], 0, 0, 0);
-      }
-    }
-    // R = beta (v - gamma P_k) in the accumulator layout
-#pragma unroll
-    for (int mt = 0; mt < NT; ++mt)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int j = mt * 16 + 4 * lg + q;
-        uint32_t vb = vraw[mt][q];
-        __asm__("" : "+v"(vb));  // keeps the widening here, not next to the load
-        rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float(vb << 16) - s_gamma[j] * pacc[NT + mt][q]) : 0.f;
-      }
-  }
-  __syncthreads();  // T complete
-  if (!cols_live) return;
-
-  // ---- U = T R, then O = Gamma P_q + Attn U, on the matrix cores; A
-  //      fragments are rows j = 16 mt + lc, columns 16 ks + 4 lg .. + 3
-  s16x4 rhi[NT], rlo[NT];
-#pragma unroll
-  for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
-  f32x4 uacc[NT];
-#pragma unroll
-  for (int mt = 0; mt < NT; ++mt) {
-    uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks <= mt; ++ks) {
-      const f32x4 tv = *reinterpret_cast<const f32x4 *>(tb + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
-      s16x4 th, tlo;
-      split4(tv, th, tlo);
-      uacc[mt] = mfma16_split(th, tlo, rhi[ks], rlo[ks], uacc[mt]);
-    }
-  }
-  s16x4 uhi[NT], ulo[NT];
-#pragma unroll
-  for (int mt = 0; mt < NT; ++mt) split4(uacc[mt], uhi[mt], ulo[mt]);
-  // outputs and corrected values of node j at ((b n + j) H + h) dv + col;
-  // rows past the last node fall outside the descriptors (the whole offset
-  // is carried per lane, where the range check applies) and are dropped
+  // ---- one V-tile: [A] delayed state update, write-back, hi/lo split,
+  //      P = [Q; K] H0 and R on the column waves (the next tile's state is
+  //      already in flight, the setup wave gathers its records); barrier;
+  //      [B] U = T R, O = Gamma P_q + Attn U and the stores.
   const uint32_t obytes = ((uint32_t)(n - 1) * nstride + dv) * 4;
   const rsrc_t orr = make_rsrc(a.out + (nbase * H + h) * dv, obytes);
   const rsrc_t urr = make_rsrc(a.fu + (nbase * H + h) * dv, obytes);
-  const uint32_t ov = (4 * lg * nstride + col) * 4;
+  auto step = [&](int i, float (&hf)[KS][8], float (&hn)[KS][8]) {
+    const int t = t0 + i;
+    const bool more = i + 1 < cnt;
+    const bool cols_live = live(t);
+    const int col = t * kTileCols + ucol;
+    const uint32_t sv = (uint32_t)(8 * lg * dv + col) * 4;
+    const float *pu = s_pu + (TPW > 1 ? (i & 1) : 0) * kPMax * kTileCols;
+    if (TPW > 1 && w == kSetup && a.has_pending && more) gather_u(t + 1, (i + 1) & 1);
+
+    // accumulator layout: lane (lg, lc) holds rows 4 lg .. 4 lg + 3 of each
+    // 16-row tile, column lc
+    f32x4 pacc[MT];
 #pragma unroll
-  for (int mt = 0; mt < NT; ++mt) {
-    f32x4 oacc = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < MT; ++mt) pacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 rreg[NT];
+    if (cols_live) {
+      const int ps = plen < kPMax ? plen : kPMax;
+      const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
+      const int pn = a.has_pending ? a.pend.n : 1;
+      if (a.has_pending) {
+        // the whole tile has normally landed by now: step-major, one LDS
+        // round trip per step
+        for (int st = 0; st < ps; ++st) {
+          const float al = s_palpha[st];
+          const float uv = pu[st * kTileCols + ucol];
+          constexpr int KC = KS < 2 ? KS : 2;  // K-steps per LDS round trip
 #pragma unroll
-    for (int ks = 0; ks <= mt; ++ks) {
-      const f32x4 av = *reinterpret_cast<const f32x4 *>(ab + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
-      s16x4 ah, alo;
-      split4(av, ah, alo);
-      oacc = mfma16_split(ah, alo, uhi[ks], ulo[ks], oacc);
+          for (int k0 = 0; k0 < KS; k0 += KC) {
+            bf16x8 kv[KC];
+#pragma unroll
+            for (int c = 0; c < KC; ++c) kv[c] = *reinterpret_cast<const bf16x8 *>(s_pk + st * DK + (k0 + c) * 32 + 8 * lg);
+#pragma unroll
+            for (int c = 0; c < KC; ++c)
+#pragma unroll
+              for (int e = 0; e < 8; ++e)
+                hf[k0 + c][e] = apply_factor(hf[k0 + c][e], al, static_cast<float>(kv[c][e]), uv);
+          }
+        }
+        // paths longer than the LDS stage read their records directly
+        for (int st = kPMax; st < plen; ++st) {
+          const int node = a.pend.path[(size_t)b * pn + st];
+          const size_t r = ((size_t)b * pn + node) * H + h;
+          const float al = a.pend.alpha[r];
+          const float uv = a.pend.u[r * dv + col];
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            float kr[8];
+            load_f32<8>(pkg + r * DK + ks * 32 + 8 * lg, kr);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, kr[e], uv);
+          }
+        }
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) buf_store_f32<kPolicyStream>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
+      }
+      // hi/lo split and P = [Q; K] H0, K-step by K-step as the tile lands
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        bf16x8 bhi, blo;
+        split8(hf[ks], bhi, blo);
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
+          pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pacc[mt], 0, 0, 0);
+          pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pacc[mt], 0, 0, 0);
+        }
+      }
+      // R = beta (v - gamma P_k) in the accumulator layout (the row base is
+      // rebuilt per tile: hoisted out of the tile loop it only gets spilled)
+      int rb = 4 * lg;
+      __asm__("" : "+v"(rb));
+#pragma unroll
+      for (int mt = 0; mt < NT; ++mt)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = mt * 16 + rb + q;
+          uint32_t vb = vraw[mt][q];
+          __asm__("" : "+v"(vb));  // keeps the widening here, not next to the load
+          rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float(vb << 16) - s_gamma[j] * pacc[NT + mt][q]) : 0.f;
+        }
     }
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int j = mt * 16 + 4 * lg + q;
-      const uint32_t vo = ov + (uint32_t)(mt * 16 + q) * nstride * 4;
-      buf_store_f32<kPolicyStream>(uacc[mt][q], urr, vo, 0);
-      buf_store_f32<kPolicyStream>(__builtin_fmaf(s_gamma[j], pacc[mt][q], oacc[q]), orr, vo, 0);
+    // the next tile's state and values go out now, while this tile's U, O
+    // and stores are computed: its state registers are free since the split,
+    // its values since R
+    if (TPW > 1 && more && live(t + 1)) {
+      load_state(t + 1, hn);
+      load_values(t + 1, vraw);
     }
-  }
+    if (TPW > 1 && w == kSetup) __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // the next tile's records have landed
+    __syncthreads();  // T complete; the next tile's records are visible
+    if (cols_live) {  // no early return: every wave takes every later barrier
+      // ---- U = T R, then O = Gamma P_q + Attn U, on the matrix cores; A
+      //      fragments are rows j = 16 mt + lc, columns 16 ks + 4 lg .. + 3
+      s16x4 rhi[NT], rlo[NT];
+#pragma unroll
+      for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
+      f32x4 uacc[NT];
+#pragma unroll
+      for (int mt = 0; mt < NT; ++mt) {
+        uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks <= mt; ++ks) {
+          const f32x4 tv = *reinterpret_cast<const f32x4 *>(tb + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
+          s16x4 th, tlo;
+          split4(tv, th, tlo);
+          uacc[mt] = mfma16_split(th, tlo, rhi[ks], rlo[ks], uacc[mt]);
+        }
+      }
+      s16x4 uhi[NT], ulo[NT];
+#pragma unroll
+      for (int mt = 0; mt < NT; ++mt) split4(uacc[mt], uhi[mt], ulo[mt]);
+      // outputs and corrected values of node j at ((b n + j) H + h) dv + col;
+      // rows past the last node fall outside the descriptors (the whole offset
+      // is carried per lane, where the range check applies) and are dropped
+      const uint32_t ov = (4 * lg * nstride + col) * 4;
+#pragma unroll
+      for (int mt = 0; mt < NT; ++mt) {
+        f32x4 oacc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks <= mt; ++ks) {
+          const f32x4 av = *reinterpret_cast<const f32x4 *>(ab + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
+          s16x4 ah, alo;
+          split4(av, ah, alo);
+          oacc = mfma16_split(ah, alo, uhi[ks], ulo[ks], oacc);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int j = mt * 16 + 4 * lg + q;
+          const uint32_t vo = ov + (uint32_t)(mt * 16 + q) * nstride * 4;
+          buf_store_f32<kPolicyStream>(uacc[mt][q], urr, vo, 0);
+          buf_store_f32<kPolicyStream>(__builtin_fmaf(s_gamma[j], pacc[mt][q], oacc[q]), orr, vo, 0);
+        }
+      }
+    }
+  };
+  // straight-line, the two state register sets trading roles (in a loop
+  // the compiler loses track of which loads a register still waits for;
+  // four tiles in a row spill)
+  static_assert(TPW == 1 || TPW == 2, "tiles per workgroup");
+  step(0, hfa, hfb);
+  if constexpr (TPW == 2) step(1, hfb, hfa);
 }
 
 constexpr size_t kMaxLds = 160 * 1024;
 constexpr size_t kDefaultLds = 64 * 1024;
 
-template <int DK, int NP>
+template <int DK, int NP, int CW, int TPW>
 hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
-  const size_t lds = Layout<DK, NP>::kBytes;
+  using L = Layout<DK, NP, CW, TPW>;
+  const size_t lds = L::kBytes;
   if (lds > kMaxLds) return hipErrorInvalidConfiguration;
-  auto kern = verify_tile_kernel<DK, NP>;
+  auto kern = verify_tile_kernel<DK, NP, CW, TPW>;
   if (lds > kDefaultLds) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  const int ntiles = (a.dv + kTileCols - 1) / kTileCols;
-  const dim3 grid((unsigned)((size_t)a.B * a.H * ntiles));
-  hipLaunchKernelGGL(kern, grid, dim3(kThreads), lds, s, a);
+  const int ntiles = (a.dv + L::kTileCols - 1) / L::kTileCols;
+  const dim3 grid((unsigned)((size_t)a.B * a.H * ((ntiles + TPW - 1) / TPW)));
+  hipLaunchKernelGGL(kern, grid, dim3((CW + 1) * kWave), lds, s, a);
   return hipGetLastError();
 }
 
 template <int DK>
 hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
-  if (a.n <= 16) return launch_np<DK, 16>(a, s);
-  if (a.n <= 32) return launch_np<DK, 32>(a, s);
-  return launch_np<DK, 64>(a, s);
+  if (a.n <= 16) return launch_np<DK, 16, 4, 1>(a, s);
+  if (a.n <= 32) return launch_np<DK, 32, 4, 1>(a, s);
+  // large trees: two V-tiles per workgroup -- topology, Grams and T serve
+  // both, and the second tile's state loads overlap the first tile's U, O
+  // and stores
+  if constexpr (DK <= 128) {
+    if (((a.dv + kWaveCols * 4 - 1) / (kWaveCols * 4)) % 2 == 0) return launch_np<DK, 64, 4, 2>(a, s);
+  }
+  return launch_np<DK, 64, 4, 1>(a, s);
 }
 
 }  // namespace
