@@ -55,6 +55,7 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int kWaveCols = 16;                    // state columns per column wave
 constexpr int kPMax = 8;                          // pending steps staged in LDS
 constexpr int kBP = 20;                           // fp32 row pitch of a 16x16 block
+constexpr int kZ = 8;                             // root paths up to this depth solve T in registers
 
 template <int DK, int NP, int CW, int TPW>
 struct Layout {
@@ -220,6 +221,7 @@ void verify_tile_kernel(VerifyArgs a) {
   int p = -1;      // setup wave, lane j: parent of node j
   float al = 1.f;  // setup wave, lane j: alpha_j
   int nodec = 0;   // setup wave, lane t: node of pending step t (clamped into the store)
+  int maxd = 0;    // setup wave: the deepest root path (wave-uniform)
   if (w == kSetup) {
     for (int c = l; c < (L::kT + L::kAt) / 16; c += kWave) reinterpret_cast<uint4 *>(tb)[c] = make_uint4(0, 0, 0, 0);
     const bf16 *qg = static_cast<const bf16 *>(a.q);
@@ -277,6 +279,9 @@ void verify_tile_kernel(VerifyArgs a) {
         const int y = __shfl_up(incl, o);
         if (l >= o) incl += y;
       }
+      maxd = d;
+#pragma unroll
+      for (int o = 1; o < kWave; o <<= 1) maxd = max(maxd, __shfl_xor(maxd, o));
       if (live) {
         s_anc[l] = m;
         s_depth[l] = d;
@@ -403,25 +408,61 @@ void verify_tile_kernel(VerifyArgs a) {
   __syncthreads();
 
   if (w == kSetup) {
-    // ---- T = (I + Lk)^-1, row j along P(j), deepest ancestor first:
-    //      T_jj = 1,  T_ja = - sum_{e in P(j), a < e} T_je Lk_ea
+    // ---- T = (I + Lk)^-1, one lane per row j.  With p_0 .. p_{d-1} = j the
+    //      root path of j and x_t = T_{j p_t}:  x_{d-1} = 1,
+    //      x_t = - sum_{u > t} x_u Lk_{p_u p_t}.
     if (l < n) {
       const int j = l;
       const uint64_t m = s_anc[j];
       tb[blk(j, j)] = 1.f;
-      uint64_t rest = m & ~(1ull << j);
-      while (rest) {
-        const int an = 63 - __builtin_clzll(rest);
-        rest &= ~(1ull << an);
-        const int ta = s_depth[an] - 1;
-        uint64_t below = m & ~((2ull << an) - 1ull);
-        float sum = 0.f;
-        while (below) {
-          const int e = __builtin_ctzll(below);
-          below &= below - 1ull;
-          sum = __builtin_fmaf(-tb[blk(j, e)], lk[s_off[e] + ta], sum);
+      if (maxd <= kZ) {
+        // push form, deepest node first: once x_u is known its terms go to
+        // every shallower position; z[k] accumulates position u - 1 - k, so
+        // the next unknown is always z[0] (registers, no LDS round trip per
+        // term; the Lk reads of one node are independent and go out together)
+        const int d = s_depth[j];
+        float z[kZ];
+#pragma unroll
+        for (int k = 0; k < kZ; ++k) z[k] = 0.f;
+        uint64_t rest = m & ~(1ull << j);
+        float xu = 1.f;
+        int pu = j;
+        for (int u = d - 1; u >= 1; --u) {
+          const float *lrow = lk + s_off[pu];
+#pragma unroll
+          for (int k0 = 0; k0 < kZ; k0 += 8) {  // eight reads per round trip
+            float lv[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) lv[k] = (u - 1 - k0 - k >= 0) ? lrow[u - 1 - k0 - k] : 0.f;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) z[k0 + k] = __builtin_fmaf(xu, lv[k], z[k0 + k]);
+          }
+          const int pn = 63 - __builtin_clzll(rest);  // p_{u-1}: deepest ancestor left
+          rest &= ~(1ull << pn);
+          xu = -z[0];
+          tb[blk(j, pn)] = xu;
+#pragma unroll
+          for (int k = 0; k + 1 < kZ; ++k) z[k] = z[k + 1];
+          z[kZ - 1] = 0.f;
+          pu = pn;
         }
-        tb[blk(j, an)] = sum;
+      } else {
+        // pull form for deep paths, deepest ancestor first:
+        //   T_ja = - sum_{e in P(j), a < e} T_je Lk_ea
+        uint64_t rest = m & ~(1ull << j);
+        while (rest) {
+          const int an = 63 - __builtin_clzll(rest);
+          rest &= ~(1ull << an);
+          const int ta = s_depth[an] - 1;
+          uint64_t below = m & ~((2ull << an) - 1ull);
+          float sum = 0.f;
+          while (below) {
+            const int e = __builtin_ctzll(below);
+            below &= below - 1ull;
+            sum = __builtin_fmaf(-tb[blk(j, e)], lk[s_off[e] + ta], sum);
+          }
+          tb[blk(j, an)] = sum;
+        }
       }
     }
     // factor records independent of the V-tile: k (from the staged rows), alpha, parent
