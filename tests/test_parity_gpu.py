@@ -142,7 +142,27 @@ def _parallel_supported(dk, dv, n, dtype):
 @pytest.mark.parametrize("route", ROUTES)
 @pytest.mark.parametrize("name", ["tiny_chain_f32", "chain8_bf16", "tree32_bf16"])
 def test_fused_round_matches_oracle_and_standalone_bitwise(name, route):
-    cfg = inputs.config(name)
+    _fused_round_check(inputs.config(name), route)
+
+
+# Larger trees over several V-tiles: two tiles per workgroup (d_v 80 with a
+# partial second tile, d_v 128), one per workgroup (d_v 192, three tiles);
+# root paths within and beyond the depth that solves T in registers.
+LARGE = [
+    inputs.Config("tree48_dv80", 95, 3, 3, 128, 80, 48, False, 6, 4, inputs.BF16, 1),
+    inputs.Config("tree48_dv128", 96, 2, 4, 128, 128, 48, False, 12, 3, inputs.BF16, 1),
+    inputs.Config("tree60_dv192", 97, 2, 2, 128, 192, 60, False, 8, 4, inputs.BF16, 1),
+    inputs.Config("tree40_dv256_dk64", 98, 2, 2, 64, 256, 40, False, 10, 3, inputs.BF16, 1),
+]
+
+
+@pytest.mark.parametrize("cfg", LARGE, ids=[c.name for c in LARGE])
+def test_fused_rounds_large_trees_many_tiles(cfg):
+    _fused_round_check(cfg, "parallel")
+
+
+def _fused_round_check(cfg, route):
+    name = cfg.name
     if route == "parallel" and not _parallel_ok(cfg):
         pytest.skip("parallel route does not support this shape")
     r0 = inputs.draw_round(cfg, 0, layers=[0])
