@@ -168,7 +168,6 @@ def main():
     torch.cuda.synchronize()
     assert int(status.abs().max()) == 0, "device reported a data error"
 
-    launches_per_step = cfg.layers * (2 if args.separate else 1)
     if args.graph:
         # One graph holds two consecutive steps (the factor stores ping-pong),
         # replayed back to back: no host work between kernel launches.
@@ -199,9 +198,10 @@ def main():
         torch.cuda.synchronize()
         t1 = time.perf_counter()
         elapsed = t1 - t0
-        # launches in a graph run back to back: the mean launch duration is the
-        # event-timed replay span over the launches it holds
-        vdur = [e0.elapsed_time(e1) / (steps * launches_per_step)]
+        # launches in a graph run back to back: the mean duration per layer
+        # (one verify, or with --separate one verify plus one commit) is the
+        # event-timed replay span over the layers it holds
+        vdur = [e0.elapsed_time(e1) / (steps * cfg.layers)]
         cdur = []
     else:
         steps = args.steps
@@ -224,11 +224,12 @@ def main():
             cdur = []
     assert int(status.abs().max()) == 0, "device reported a data error"
     ms_per_step = 1e3 * elapsed / steps
-    v_ms = float(np.mean(vdur))
+    # per layer: the fused call, or with --separate the verify (state read
+    # once) plus the standalone commit (state read and written once more)
+    v_ms = float(np.mean(vdur)) + (float(np.mean(cdur)) if cdur else 0.0)
     bytes_launch = algorithmic_bytes(cfg, rnd.length)
     if args.separate:
-        # without a pending path the verify reads the state only; commit reads and writes it
-        bytes_launch -= cfg.batch * cfg.heads * cfg.d_k * cfg.d_v * 4
+        bytes_launch += cfg.batch * cfg.heads * cfg.d_k * cfg.d_v * 4
     achieved = bytes_launch / (v_ms * 1e-3) / 1e9
     nodes = cfg.batch * cfg.n_nodes * cfg.layers * steps
     value = nodes / elapsed
@@ -245,7 +246,7 @@ def main():
             kernel = tj[key].get("kernel")
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "kernel": kernel or "sla verify (%s route)" % args.route,
+            "kernel": kernel or ("sla verify (%s route)%s" % (args.route, " + sla commit" if args.separate else "")),
             "algorithmic_bytes_per_launch": int(bytes_launch), "avg_launch_ms": round(v_ms, 5)}
     line = {
         "metric": METRIC, "value": round(value, 1), "unit": "nodes/s", "n_gpus": 1, "steps": steps,
@@ -258,6 +259,8 @@ def main():
                    "commit": "separate" if args.separate else "fused", "parallelism": "single-gpu",
                    "launch": "hip graph" if args.graph else "eager"},
         "hbm_gbps": round(achieved, 1),
+        # one token through every layer of the workload (one layer's node is `value`'s unit)
+        "tokens_per_s": round(cfg.batch * cfg.n_nodes * steps / elapsed, 1),
         "roofline": roof,
     }
     if cdur:
