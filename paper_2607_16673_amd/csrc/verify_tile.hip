@@ -657,8 +657,10 @@ hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
   if (a.n <= 32) return launch_np<DK, 32, 4, 1>(a, s);
   // large trees: two V-tiles per workgroup -- topology, Grams and T serve
   // both, and the second tile's state loads overlap the first tile's U, O
-  // and stores
+  // and stores; with d_v a multiple of 256, tiles of 128 columns (eight
+  // column waves), so that one workgroup covers 256 columns
   if constexpr (DK <= 128) {
+    if (a.dv % 256 == 0) return launch_np<DK, 64, 8, 2>(a, s);
     if (((a.dv + kWaveCols * 4 - 1) / (kWaveCols * 4)) % 2 == 0) return launch_np<DK, 64, 4, 2>(a, s);
   }
   return launch_np<DK, 64, 4, 1>(a, s);
