@@ -14,33 +14,35 @@
 // and the only sequential work is the small per-unit T (each lane walks its
 // own node's root path).  Only the committed state is read.
 //
-// One workgroup = one (batch b, head h, 64-column V-tile), five wavefronts:
-//   waves 0-3  own 16 state columns each.  They issue the state tile reads
-//              (in the B-fragment order of v_mfma_f32_16x16x32_bf16: 8
+// One workgroup = one (batch b, head h) unit's V-tile of CW x 16 columns
+// (CW = 4 or 8), or TPW = 2 consecutive such tiles, with CW + 1 wavefronts:
+//   waves 0 .. CW-1 own 16 state columns each.  They issue the state tile
+//              reads (in the B-fragment order of v_mfma_f32_16x16x32_bf16: 8
 //              consecutive rows of one column per 32-row K-step) and the
 //              value reads first thing.  The reads keep the default cache
 //              policy: a wave covers only half of each 128-byte line, and
 //              with a streaming hint the L2 lets the line go before the
 //              neighbouring wave asks for the other half (measured: about
-//              15% more HBM reads).  The tile is consumed
-//              K-step by K-step as it lands: pending path applied,
+//              15% more HBM reads).  Per tile: pending path applied,
 //              committed rows written back, fp32 split into bf16 hi + lo,
-//              P = [Q; K] H0 accumulated on the matrix cores.  Then
-//              R = beta (v - gamma P_k), U = T R and O = Gamma P_q + Attn U on
-//              v_mfma_f32_16x16x16bf16_1k (whose B fragment is exactly the
-//              accumulator layout holding R, then U), and the outputs.
-//   wave 4     owns no state.  It takes every read that depends on another
+//              P = [Q; K] H0 accumulated on the matrix cores K-step by
+//              K-step.  Then R = beta (v - gamma P_k), U = T R and
+//              O = Gamma P_q + Attn U on v_mfma_f32_16x16x16bf16_1k (whose B
+//              fragment is exactly the accumulator layout holding R, then U),
+//              and the outputs.  With two tiles, the second tile's reads go
+//              out once the first tile's registers are free.
+//   wave CW    owns no state.  It takes every read that depends on another
 //              read or that everything else waits for: parent row and gates
 //              -> topology, decays and compact-list offsets; the pending path
 //              with the previous round's parent row and gates -> validation;
 //              [Q; K] by direct global->LDS loads; then, while the column
-//              waves compute the Grams, the factor records the path names
-//              (also straight into LDS).  After the Grams it solves the
-//              per-node rows of T.
+//              waves compute, the factor records the path names (also
+//              straight into LDS, a second stage for a second tile).  After
+//              the Grams it solves the per-node rows of T.
 // The tree-masked Grams ([Q; K] K^T tiles that hold ancestor pairs, exact
 // bf16 products) run on the column waves; they and T are done while the
-// state tile is still in flight.  Strided global accesses go through buffer
-// descriptors (one VGPR offset per lane).
+// first tile's state is still in flight.  Strided global accesses go through
+// buffer descriptors (one VGPR offset per lane).
 #include "device.hpp"
 #include "kernels.hpp"
 
