@@ -464,3 +464,52 @@ def test_empty_pending_path_is_a_noop_commit():
     verify(torch.from_numpy(S0).cuda(), L1, o_b, new_factors(cfg))
     torch.cuda.synchronize()
     assert torch.equal(o_a, o_b)
+
+
+# ------------------------- pending path from a differently shaped round
+@pytest.mark.parametrize("route", ROUTES)
+def test_pending_from_larger_round_with_long_paths(route):
+    """Round 0: 24-node chains; the accepted paths (15, 24 and 0 steps) are
+    longer than the records staged on chip, so the column waves read the rest
+    directly.  Round 1: 16-node trees verified with round 0's path pending
+    (the previous store has 24 nodes per sequence, the new one 16)."""
+    c0 = inputs.Config("prev24", 110, 3, 4, 128, 128, 24, True, 24, 1, inputs.BF16, 1)
+    c1 = inputs.Config("next16", 111, 3, 4, 128, 128, 16, False, 5, 3, inputs.BF16, 1)
+    if route == "parallel" and not (_parallel_ok(c0) and _parallel_ok(c1)):
+        pytest.skip("parallel route does not support this shape")
+    r0 = inputs.draw_round(c0, 0, layers=[0])
+    r0.length = np.array([15, 24, 0], np.int32)
+    r0.path = np.tile(np.arange(24, dtype=np.int32), (3, 1))
+    for b, ln in enumerate(r0.length):
+        r0.path[b, ln:] = -1
+    r1 = inputs.draw_round(c1, 0, layers=[0])
+    S0 = inputs.draw_state(c0, 0)
+    L0, L1 = Layer(c0, r0, 0), Layer(c1, r1, 0)
+    f0, f1, g0, g1 = new_factors(c0), new_factors(c1), new_factors(c0), new_factors(c1)
+    out0, out1, o0, o1 = new_out(c0), new_out(c1), new_out(c0), new_out(c1)
+    say("pending from a 24-node round, %s" % route)
+    fused = torch.from_numpy(S0).cuda()
+    verify(fused, L0, out0, f0, route=route)
+    st = torch.full((3,), 99, dtype=torch.int32, device="cuda")
+    verify(fused, L1, out1, f1, pending=(f0, L0.path, L0.length), status=st, route=route)
+    sep = torch.from_numpy(S0).cuda()
+    verify(sep, L0, o0, g0, route=route)
+    B.sla_commit(sep, g0, L0.path, L0.length)
+    verify(sep, L1, o1, g1, route=route)
+    torch.cuda.synchronize()
+    assert (st.cpu().numpy() == 0).all()
+    assert torch.equal(fused, sep), "fused and standalone commit differ"
+    assert torch.equal(out1, o1), "fused and separate verification outputs differ"
+    units = [(b, h) for b in range(3) for h in range(4)]
+    S1 = oracle_commit_units(S0, r0, 0, units)
+    errS = rel_err(np.stack([fused.cpu().numpy()[b, h] for b, h in units]), np.stack([S1[u] for u in units]))
+    S1full = S0.astype(np.float64).copy()
+    for (b, h), s_ in S1.items():
+        S1full[b, h] = s_
+    ref = oracle_verify_units(S1full, r1, 0, units)
+    got = out1.cpu().numpy()
+    err = rel_err(np.stack([got[b, :, h] for b, h in units]), np.stack([ref[u] for u in units]))
+    say("pending from a 24-node round, %s: state err %.3e output err %.3e" % (route, errS, err))
+    assert errS <= 2e-3 and err <= 2e-3
+    # the empty path left sequence 2's state as it was
+    np.testing.assert_array_equal(fused.cpu().numpy()[2], S0[2])
