@@ -71,7 +71,7 @@ struct Layout {
   static constexpr int kAt = NB * kBlk;             // Attn blocks
   static constexpr int kLk = kList * 4;
   static constexpr int kPk = kPMax * DK * 2;        // pending keys (bf16)
-  static constexpr int kPu = (TPW > 1 ? 2 : 1) * kPMax * kTileCols * 4;  // pending corrected values, per tile
+  static constexpr int kPu = TPW * kPMax * kTileCols * 4;  // pending corrected values, one stage per tile
   static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 4 + 16;
   static constexpr int kBytes = kX + kT + kAt + kLk + kPk + kPu + kTopo;
 };
@@ -346,7 +346,10 @@ void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
     for (int i = 0; i < KI; ++i)
       load_lds16(pkg + ((prow + nt[i]) * H + h) * DK + ((i * kWave + l) % CH) * 8, s_pk + i * kWave * 8);
-    gather_u(t0, 0);
+    // every tile's values at once: a later tile's would otherwise be waited
+    // for on the critical path
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) gather_u(t0 + i, i);
   }
 
   // ---- tree-masked Grams over the column waves: tile (mr, na) of [Q; K] K^T holds
@@ -467,24 +470,12 @@ void verify_tile_kernel(VerifyArgs a) {
         }
       }
     }
-    // factor records independent of the V-tile: k (from the staged rows), alpha, parent
-    if (t0 == 0) {
-      bf16 *fk = static_cast<bf16 *>(a.fk);
-      for (int c = l; c < n * CH; c += kWave) {
-        const int j = c / CH, part = c % CH;
-        *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * 8) = xs[xchunk<CH>(NP + j, part)];
-      }
-      if (l < n) {
-        a.falpha[(nbase + l) * H + h] = al;
-        if (h == 0) a.fparent[nbase + l] = p;
-      }
-    }
   }
 
   // ---- one V-tile: [A] delayed state update, write-back, hi/lo split,
-  //      P = [Q; K] H0 and R on the column waves (the next tile's state is
-  //      already in flight, the setup wave gathers its records); barrier;
-  //      [B] U = T R, O = Gamma P_q + Attn U and the stores.
+  //      P = [Q; K] H0 and R on the column waves; barrier (T complete);
+  //      [B] U = T R, O = Gamma P_q + Attn U and the stores; then the next
+  //      tile's state and values go out.
   const uint32_t obytes = ((uint32_t)(n - 1) * nstride + dv) * 4;
   const rsrc_t orr = make_rsrc(a.out + (nbase * H + h) * dv, obytes);
   const rsrc_t urr = make_rsrc(a.fu + (nbase * H + h) * dv, obytes);
@@ -494,8 +485,7 @@ void verify_tile_kernel(VerifyArgs a) {
     const bool cols_live = live(t);
     const int col = t * kTileCols + ucol;
     const uint32_t sv = (uint32_t)(8 * lg * dv + col) * 4;
-    const float *pu = s_pu + (TPW > 1 ? (i & 1) : 0) * kPMax * kTileCols;
-    if (TPW > 1 && w == kSetup && a.has_pending && more) gather_u(t + 1, (i + 1) & 1);
+    const float *pu = s_pu + i * kPMax * kTileCols;
 
     // accumulator layout: lane (lg, lc) holds rows 4 lg .. 4 lg + 3 of each
     // 16-row tile, column lc
@@ -578,8 +568,21 @@ void verify_tile_kernel(VerifyArgs a) {
       load_state(t + 1, hn);
       load_values(t + 1, vraw);
     }
-    if (TPW > 1 && w == kSetup) __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // the next tile's records have landed
-    __syncthreads();  // T complete; the next tile's records are visible
+    __syncthreads();  // T complete
+    // factor records independent of the V-tile -- k (from the staged rows),
+    // alpha, parent -- while the column waves compute the first tile's
+    // products (off the path to the barrier above)
+    if (w == kSetup && i == 0 && t0 == 0) {
+      bf16 *fk = static_cast<bf16 *>(a.fk);
+      for (int c = l; c < n * CH; c += kWave) {
+        const int j = c / CH, part = c % CH;
+        *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * 8) = xs[xchunk<CH>(NP + j, part)];
+      }
+      if (l < n) {
+        a.falpha[(nbase + l) * H + h] = al;
+        if (h == 0) a.fparent[nbase + l] = p;
+      }
+    }
     if (cols_live) {  // no early return: every wave takes every later barrier
       // ---- U = T R, then O = Gamma P_q + Attn U, on the matrix cores; A
       //      fragments are rows j = 16 mt + lc, columns 16 ks + 4 lg .. + 3
