@@ -13,53 +13,120 @@ namespace sla {
 namespace {
 
 constexpr int kCommitThreads = 256;
+constexpr int kCommitCols = 64;   // state columns per workgroup
+constexpr int kCommitStage = 8;   // path records staged in LDS; longer paths read the rest directly
 
-template <typename T>
+// One workgroup = one (b, h) unit's 64-column slab, all d_k rows.  Thread t
+// owns float4 column group t % 16 of rows t / 16 + 16 r: 16 threads cover a
+// 256-byte row segment, so every access is whole 128-byte lines.  The slab
+// is read first thing, before the path is known; wave 0 reads the path, the
+// parent row and the gates whole (validation takes no dependent read), then
+// gathers the records the path names straight into LDS.  An invalid path
+// reports its status and leaves the state untouched.
+template <typename T, int DK>
 __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a) {
-  __shared__ int s_err;
-  __shared__ int s_node[SLA_MAX_NODES];
-  __shared__ float s_alpha[SLA_MAX_NODES];
+  constexpr int R = DK / 16;  // float4 groups per thread
+  __shared__ int s_err, s_len;
+  __shared__ float s_alpha[kCommitStage];
+  __shared__ __attribute__((aligned(16))) unsigned char s_kraw[kCommitStage * DK * sizeof(T)];
+  __shared__ __attribute__((aligned(16))) float s_u[kCommitStage][kCommitCols];
+  const T *s_k = reinterpret_cast<const T *>(s_kraw);  // [kCommitStage][DK]
   const int tid = threadIdx.x;
-  const int H = a.H, dk = a.dk, dv = a.dv, n = a.n;
-  const int b = blockIdx.x / H;
-  const int h = blockIdx.x % H;
-  const int32_t *path = a.path + (size_t)b * n;
-  if (tid < kWave) {
-    const int len = a.len[b];
-    const int e = check_path(a.parent + (size_t)b * n, n, path, len, tid);
-    if (tid == 0) s_err = e;
-    if (e == SLA_OK && tid < len) {
-      s_node[tid] = path[tid];
-      s_alpha[tid] = a.alpha[((size_t)b * n + path[tid]) * H + h];
+  const int w = tid / kWave, l = tid % kWave;
+  const int H = a.H, dv = a.dv, n = a.n;
+  const int nslab = (dv + kCommitCols - 1) / kCommitCols;
+  int wid = blockIdx.x;
+  const int slab = wid % nslab;
+  wid /= nslab;
+  const int h = wid % H;
+  const int b = wid / H;
+  const size_t rowp = (size_t)b * n;
+
+  // wave 0: everything the path check needs, ahead of its slab reads
+  int len = 0, node = -1, par = -2;
+  float al = 0.f;
+  if (w == 0) {
+    len = a.len[b];
+    node = l < n ? a.path[rowp + l] : -1;
+    par = l < n ? a.parent[rowp + l] : -2;
+    al = l < n ? a.alpha[(rowp + l) * H + h] : 0.f;
+  }
+  // the slab, before the path is known
+  const int cg = slab * kCommitCols + (tid % 16) * 4;  // first column of this thread's float4
+  const bool cl = cg < dv;
+  float *st = a.state + ((size_t)b * H + h) * DK * dv;
+  float4 x[R];
+  if (cl) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) x[r] = *reinterpret_cast<const float4 *>(st + (size_t)(tid / 16 + 16 * r) * dv + cg);
+  }
+  if (w == 0) {
+    // step t is node path[t], whose parent must be path[t - 1] (-1 for t = 0)
+    const bool inrange = node >= 0 && node < n;
+    const int nodec = inrange ? node : 0;
+    int prev = __shfl_up(node, 1);
+    if (l == 0) prev = -1;
+    const int pp = __shfl(par, nodec);
+    const float pa = __shfl(al, nodec);
+    const bool bad = (len < 0 || len > n) || (l < len && (!inrange || pp != prev));
+    const int err = wave_any(bad) ? SLA_ERR_PATH : SLA_OK;
+    if (l == 0) {
+      s_err = err;
+      s_len = len;
     }
+    if (l < kCommitStage) s_alpha[l] = pa;
+    if (h == 0 && slab == 0 && l == 0 && a.status) a.status[b] = err;
+    // records of the first steps (indices clamped into the store): key rows
+    // and this slab's corrected values, straight into LDS
+    const T *fk = static_cast<const T *>(a.k);
+    constexpr int KC = DK * (int)sizeof(T) / 16;  // 16-byte chunks per key row
+    constexpr int KI = kCommitStage * KC / kWave;
+    int nt[KI];  // shuffles first: an LDS instruction after an LDS-DMA load waits for it
+#pragma unroll
+    for (int i = 0; i < KI; ++i) nt[i] = __shfl(nodec, (i * kWave + l) / KC);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < KI; ++i)
+      load_lds16(fk + ((rowp + nt[i]) * H + h) * DK + ((i * kWave + l) % KC) * (16 / sizeof(T)), s_kraw + i * kWave * 16);
+#pragma unroll
+    for (int t = 0; t < kCommitStage; ++t) {
+      const int ntt = __builtin_amdgcn_readlane(nodec, t);
+      const int c = slab * kCommitCols + l;
+      load_lds4(a.u + ((rowp + ntt) * H + h) * dv + (c < dv ? c : dv - 1), &s_u[t][0]);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // the records have landed
   }
   __syncthreads();
-  const int err = s_err;
-  if (h == 0 && tid == 0 && a.status) a.status[b] = err;
-  if (err != SLA_OK) return;
-  const int len = a.len[b];
-  if (len == 0) return;
-
-  const T *fk = static_cast<const T *>(a.k);
-  float *st = a.state + ((size_t)b * H + h) * dk * dv;
-  const int cq = dv / 4;  // float4 columns per row
-  const int total = dk * cq;
-  for (int f = tid; f < total; f += kCommitThreads) {
-    const int i = f / cq;
-    const int c = (f - i * cq) * 4;
-    float4 x = *reinterpret_cast<const float4 *>(st + (size_t)i * dv + c);
-    for (int t = 0; t < len; ++t) {
-      const size_t s = ((size_t)b * n + s_node[t]) * H + h;
-      const float al = s_alpha[t];
-      const float ki = to_f32(fk[s * dk + i]);
-      const float4 u = *reinterpret_cast<const float4 *>(a.u + s * dv + c);
-      x.x = apply_factor(x.x, al, ki, u.x);
-      x.y = apply_factor(x.y, al, ki, u.y);
-      x.z = apply_factor(x.z, al, ki, u.z);
-      x.w = apply_factor(x.w, al, ki, u.w);
+  if (s_err != SLA_OK || !cl) return;
+  len = s_len;
+  const int cs = (tid % 16) * 4;  // column within the slab
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int i = tid / 16 + 16 * r;
+    for (int t = 0; t < len && t < kCommitStage; ++t) {
+      const float alt = s_alpha[t];
+      const float ki = to_f32(s_k[t * DK + i]);
+      const float4 u = *reinterpret_cast<const float4 *>(&s_u[t][cs]);
+      x[r].x = apply_factor(x[r].x, alt, ki, u.x);
+      x[r].y = apply_factor(x[r].y, alt, ki, u.y);
+      x[r].z = apply_factor(x[r].z, alt, ki, u.z);
+      x[r].w = apply_factor(x[r].w, alt, ki, u.w);
     }
-    *reinterpret_cast<float4 *>(st + (size_t)i * dv + c) = x;
+    // paths longer than the stage read their records directly
+    for (int t = kCommitStage; t < len; ++t) {
+      const size_t s = (rowp + a.path[rowp + t]) * H + h;
+      const float alt = a.alpha[s];
+      const float ki = to_f32(static_cast<const T *>(a.k)[s * DK + i]);
+      const float4 u = *reinterpret_cast<const float4 *>(a.u + s * dv + cg);
+      x[r].x = apply_factor(x[r].x, alt, ki, u.x);
+      x[r].y = apply_factor(x[r].y, alt, ki, u.y);
+      x[r].z = apply_factor(x[r].z, alt, ki, u.z);
+      x[r].w = apply_factor(x[r].w, alt, ki, u.w);
+    }
   }
+  if (len == 0) return;
+#pragma unroll
+  for (int r = 0; r < R; ++r) *reinterpret_cast<float4 *>(st + (size_t)(tid / 16 + 16 * r) * dv + cg) = x[r];
 }
 
 __global__ __launch_bounds__(kWave) void topology_kernel(TopologyArgs a) {
@@ -77,15 +144,28 @@ __global__ __launch_bounds__(kWave) void topology_kernel(TopologyArgs a) {
   a.n_children[r + lane] = t.n_children;
 }
 
+template <typename T, int DK>
+hipError_t launch_commit_dk(const CommitArgs &a, hipStream_t s) {
+  auto kern = commit_kernel<T, DK>;
+  const dim3 grid((unsigned)((size_t)a.B * a.H * ((a.dv + kCommitCols - 1) / kCommitCols)));
+  hipLaunchKernelGGL(kern, grid, dim3(kCommitThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_commit_t(const CommitArgs &a, hipStream_t s) {
+  switch (a.dk) {
+    case 64: return launch_commit_dk<T, 64>(a, s);
+    case 128: return launch_commit_dk<T, 128>(a, s);
+    case 256: return launch_commit_dk<T, 256>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_commit(const CommitArgs &a, int dtype, hipStream_t s) {
-  const dim3 grid((unsigned)((size_t)a.B * a.H));
-  if (dtype == SLA_DTYPE_BF16)
-    hipLaunchKernelGGL(commit_kernel<bf16>, grid, dim3(kCommitThreads), 0, s, a);
-  else
-    hipLaunchKernelGGL(commit_kernel<float>, grid, dim3(kCommitThreads), 0, s, a);
-  return hipGetLastError();
+  return dtype == SLA_DTYPE_BF16 ? launch_commit_t<bf16>(a, s) : launch_commit_t<float>(a, s);
 }
 
 hipError_t launch_topology(const TopologyArgs &a, hipStream_t s) {

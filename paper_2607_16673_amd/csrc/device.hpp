@@ -81,6 +81,23 @@ __device__ __forceinline__ float buf_load_bf16(rsrc_t r, uint32_t voff, uint32_t
   return __uint_as_float((uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, kPolicyDefault) << 16);
 }
 
+// ------------------------------------------------------ direct LDS loads
+// global_load_lds: each lane's bytes go straight from memory to LDS, at
+// lds_wave_base + size * lane (the base is wave-uniform); no registers are
+// involved.  An LDS instruction issued after one of these waits for it.
+// Kernels call these helpers, never the builtin itself: a kernel template
+// whose body names the builtin gets no host-side launch stub (the link then
+// fails on an undefined kernel symbol).
+typedef __attribute__((address_space(3))) void lds_void;
+
+__device__ __forceinline__ void load_lds16(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)(lds_wave_base), 16, 0, 0);
+}
+
+__device__ __forceinline__ void load_lds4(const void *g, void *lds_wave_base) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void *)(lds_wave_base), 4, 0, 0);
+}
+
 // ------------------------------------------------------- rank-one update
 // One accepted (or materialised) node a advances the transposed state
 // H = S^T elementwise:  H[i][c] <- alpha_a * H[i][c] + k_a[i] * u_a[c].

@@ -52,7 +52,6 @@ namespace {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) short s16x4;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
-typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kWaveCols = 16;                    // state columns per column wave
 constexpr int kPMax = 8;                          // pending steps staged in LDS
@@ -81,17 +80,6 @@ struct Layout {
 template <int CH>
 __device__ __forceinline__ int xchunk(int row, int c) {
   return row * CH + (c ^ (row & 7));
-}
-
-// Each lane's 16 bytes land at lds_wave_base + 16 * lane (the base is
-// wave-uniform); no registers are involved.
-__device__ __forceinline__ void load_lds16(const void *g, void *lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void *)(lds_wave_base), 16, 0, 0);
-}
-
-// Each lane's 4 bytes land at lds_wave_base + 4 * lane.
-__device__ __forceinline__ void load_lds4(const void *g, void *lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void *)(lds_wave_base), 4, 0, 0);
 }
 
 // s_waitcnt immediate that waits until at most `n` vector memory operations
