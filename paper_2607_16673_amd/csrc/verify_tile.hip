@@ -477,9 +477,9 @@ void verify_tile_kernel(VerifyArgs a) {
 
     // accumulator layout: lane (lg, lc) holds rows 4 lg .. 4 lg + 3 of each
     // 16-row tile, column lc
-    f32x4 pacc[MT];
+    f32x4 pq[NT];  // P_q = Q H0, accumulator layout
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) pacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < NT; ++mt) pq[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
     f32x4 rreg[NT];
     if (cols_live) {
       const int ps = plen < kPMax ? plen : kPMax;
@@ -523,20 +523,25 @@ void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) buf_store_f32<kPolicyStream>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
       }
-      // hi/lo split and P = [Q; K] H0, K-step by K-step as the tile lands
+      // P_k = K H0 first (hi/lo split, K-step by K-step as the tile lands),
+      // so that R = beta (v - gamma P_k) takes its place before P_q is built:
+      // the two halves of P are never held at once
+      f32x4 pk[NT];
+#pragma unroll
+      for (int mt = 0; mt < NT; ++mt) pk[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         bf16x8 bhi, blo;
         split8(hf[ks], bhi, blo);
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt) {
-          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
-          pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pacc[mt], 0, 0, 0);
-          pacc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pacc[mt], 0, 0, 0);
+        for (int mt = 0; mt < NT; ++mt) {
+          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + mt * 16 + lc, ks * 4 + lg));
+          pk[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pk[mt], 0, 0, 0);
+          pk[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pk[mt], 0, 0, 0);
         }
       }
-      // R = beta (v - gamma P_k) in the accumulator layout (the row base is
-      // rebuilt per tile: hoisted out of the tile loop it only gets spilled)
+      // R in the accumulator layout (the row base is rebuilt per tile:
+      // hoisted out of the tile loop it only gets spilled)
       int rb = 4 * lg;
       __asm__("" : "+v"(rb));
 #pragma unroll
@@ -546,8 +551,19 @@ void verify_tile_kernel(VerifyArgs a) {
           const int j = mt * 16 + rb + q;
           uint32_t vb = vraw[mt][q];
           __asm__("" : "+v"(vb));  // keeps the widening here, not next to the load
-          rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float(vb << 16) - s_gamma[j] * pacc[NT + mt][q]) : 0.f;
+          rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float(vb << 16) - s_gamma[j] * pk[mt][q]) : 0.f;
         }
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        bf16x8 bhi, blo;
+        split8(hf[ks], bhi, blo);
+#pragma unroll
+        for (int mt = 0; mt < NT; ++mt) {
+          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
+          pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pq[mt], 0, 0, 0);
+          pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pq[mt], 0, 0, 0);
+        }
+      }
     }
     // the next tile's state and values go out now, while this tile's U, O
     // and stores are computed: its state registers are free since the split,
@@ -611,7 +627,7 @@ void verify_tile_kernel(VerifyArgs a) {
           const int j = mt * 16 + 4 * lg + q;
           const uint32_t vo = ov + (uint32_t)(mt * 16 + q) * nstride * 4;
           buf_store_f32<kPolicyStream>(uacc[mt][q], urr, vo, 0);
-          buf_store_f32<kPolicyStream>(__builtin_fmaf(s_gamma[j], pacc[mt][q], oacc[q]), orr, vo, 0);
+          buf_store_f32<kPolicyStream>(__builtin_fmaf(s_gamma[j], pq[mt][q], oacc[q]), orr, vo, 0);
         }
       }
     }
