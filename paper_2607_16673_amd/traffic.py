@@ -66,6 +66,9 @@ def _rows(dirname: str, counter: str):
     files = glob.glob(os.path.join(dirname, "**", "*counter_collection.csv"), recursive=True)
     if not files:
         raise FileNotFoundError("no counter_collection.csv under %s" % dirname)
+    if len(files) > 1:
+        # one pass is one process: more files mean results of several runs mixed in one folder
+        raise RuntimeError("%d counter files under %s; give each pass a fresh folder" % (len(files), dirname))
     out = []
     for fn in files:
         with open(fn, newline="") as f:
