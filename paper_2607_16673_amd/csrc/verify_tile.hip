@@ -126,7 +126,7 @@ __device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x
 // tile state, accumulators and LDS allow a fourth resident workgroup per CU,
 // else whatever the allocation needs.
 template <int DK, int NP, int TPW>
-constexpr int kMinWaves = (DK <= 128 && NP <= 16 && TPW == 1) ? 6 : 1;
+constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
 
 template <int DK, int NP, int CW, int TPW>
 __global__ __launch_bounds__((CW + 1) * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
@@ -660,8 +660,26 @@ hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
 template <int DK>
 hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
+  // small trees: two V-tiles of a unit per workgroup once single tiles would
+  // fill every CU's four workgroup slots twice over.  The launch is then one
+  // round of long-lived workgroups instead of two, and q, k, topology, Grams
+  // and T serve both tiles.  Below that, single tiles keep more workgroups
+  // (and CUs) busy.
+  if constexpr (DK <= 128) {
+    const int ntiles = (a.dv + kWaveCols * 4 - 1) / (kWaveCols * 4);
+    if (a.n <= 32 && ntiles % 2 == 0 && (size_t)a.B * a.H * ntiles >= (size_t)8 * device_cus())
+      return a.n <= 16 ? launch_np<DK, 16, 4, 2>(a, s) : launch_np<DK, 32, 4, 2>(a, s);
+  }
   if (a.n <= 16) return launch_np<DK, 16, 4, 1>(a, s);
   if (a.n <= 32) return launch_np<DK, 32, 4, 1>(a, s);
   // large trees: two V-tiles per workgroup -- topology, Grams and T serve

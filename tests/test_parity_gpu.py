@@ -147,12 +147,19 @@ def test_fused_round_matches_oracle_and_standalone_bitwise(name, route):
 
 # Larger trees over several V-tiles: two tiles per workgroup (d_v 80 with a
 # partial second tile, d_v 128), one per workgroup (d_v 192, three tiles);
-# root paths within and beyond the depth that solves T in registers.
+# root paths within and beyond the depth that solves T in registers; and
+# small trees at batch sizes where they pair V-tiles too.
 LARGE = [
     inputs.Config("tree48_dv80", 95, 3, 3, 128, 80, 48, False, 6, 4, inputs.BF16, 1),
     inputs.Config("tree48_dv128", 96, 2, 4, 128, 128, 48, False, 12, 3, inputs.BF16, 1),
     inputs.Config("tree60_dv192", 97, 2, 2, 128, 192, 60, False, 8, 4, inputs.BF16, 1),
     inputs.Config("tree40_dv256_dk64", 98, 2, 2, 64, 256, 40, False, 10, 3, inputs.BF16, 1),
+    # batches large enough that small trees take two V-tiles per workgroup
+    # (13 and 27 nodes: ragged against the 16- and 32-row node blocks; paths
+    # up to 12 deep, past the records staged on chip; d_v 256: two pairs)
+    inputs.Config("pair_tree13", 112, 64, 16, 128, 128, 13, False, 5, 3, inputs.BF16, 1),
+    inputs.Config("pair_tree27_deep", 113, 64, 16, 128, 128, 27, False, 12, 3, inputs.BF16, 1),
+    inputs.Config("pair_tree16_dv256", 114, 32, 16, 128, 256, 16, False, 5, 3, inputs.BF16, 1),
 ]
 
 
