@@ -22,6 +22,7 @@ struct VerifyArgs {
   int32_t B, H, dk, dv, n;
   bool chain;
   bool has_pending;
+  bool late_state;  // parallel route: issue the state reads after the first barrier
   float *state;
   PendingArgs pend;
   const void *q, *k, *v;

@@ -203,7 +203,7 @@ void verify_tile_kernel(VerifyArgs a) {
   float hfa[KS][8], hfb[KS][8];  // hfb: the next tile's state (prefetching form only)
   uint32_t vraw[NT][4];  // bf16 bit patterns, widened where they are used
   if (live(t0)) {
-    load_state(t0, hfa);
+    if (!a.late_state) load_state(t0, hfa);
     load_values(t0, vraw);
   }
 
@@ -305,6 +305,9 @@ void verify_tile_kernel(VerifyArgs a) {
   __syncthreads();
   const int err = s_misc[0];
   if (err != SLA_OK) return;
+  // many rounds of workgroups: the state goes out only now, behind the small
+  // reads the setup wave waits for
+  if (a.late_state && live(t0)) load_state(t0, hfa);
   const int plen = s_misc[1];
 
   // ---- setup wave: records of the first kPMax path nodes, gathered straight
@@ -643,6 +646,22 @@ void verify_tile_kernel(VerifyArgs a) {
 constexpr size_t kMaxLds = 160 * 1024;
 constexpr size_t kDefaultLds = 64 * 1024;
 
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
+// The state reads of a workgroup normally go out first, so that they overlap
+// the setup wave's dependent reads.  When the launch holds at least
+// kLateRounds rounds of workgroups (counting kSlotsPerCu resident per CU),
+// they go out after the first barrier instead: measured 4.5% faster on the
+// 1-node decode chain at batch 256, 1% slower at one round.
+constexpr int kLateRounds = 4;
+constexpr int kSlotsPerCu = 4;
+
 template <int DK, int NP, int CW, int TPW>
 hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
   using L = Layout<DK, NP, CW, TPW>;
@@ -655,17 +674,11 @@ hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
     if (e != hipSuccess) return e;
   }
   const int ntiles = (a.dv + L::kTileCols - 1) / L::kTileCols;
-  const dim3 grid((unsigned)((size_t)a.B * a.H * ((ntiles + TPW - 1) / TPW)));
-  hipLaunchKernelGGL(kern, grid, dim3((CW + 1) * kWave), lds, s, a);
+  const size_t groups = (size_t)a.B * a.H * ((ntiles + TPW - 1) / TPW);
+  VerifyArgs b = a;
+  b.late_state = groups >= (size_t)kLateRounds * kSlotsPerCu * device_cus();
+  hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3((CW + 1) * kWave), lds, s, b);
   return hipGetLastError();
-}
-
-int device_cus() {
-  int dev = 0, cus = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
-      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
-    return 256;
-  return cus;
 }
 
 template <int DK>
