@@ -52,28 +52,31 @@ def algorithmic_bytes(cfg, pending_len):
     return state + draft + out + factors + pend
 
 
-def cpu_baseline(cfg, rounds, states, budget_s=12.0):
+def cpu_baseline(cfg, rounds, states, budget_s=10.0):
     """The fp64 oracle (verify + commit by definition) on the host cores, on
-    whole layers of the same workload until about budget_s of CPU time."""
+    whole layers of the same workload, cycling through the layers until about
+    budget_s of CPU time has passed."""
     import oracle
 
     r0 = rounds
     t0 = time.perf_counter()
-    layers = 0
-    for layer in range(cfg.layers):
+    passes = 0
+    while True:
+        layer = passes % cfg.layers
         out, st = oracle.verify(states[layer], r0.q32[layer], r0.k32[layer], r0.v32[layer], r0.alpha[layer],
                                 r0.beta[layer], r0.parent)
         S1, st2 = oracle.commit(states[layer], r0.k32[layer], r0.v32[layer], r0.alpha[layer],
                                 r0.beta[layer], r0.parent, r0.path, r0.length)
         assert (st == 0).all() and (st2 == 0).all()
-        layers += 1
+        passes += 1
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = time.perf_counter() - t0
-    nodes = layers * cfg.batch * cfg.n_nodes
+    nodes = passes * cfg.batch * cfg.n_nodes
     return {"value": nodes / dt, "unit": "nodes/s", "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": "%d of %d layers of the %s workload (all %d sequences x %d heads), verify + commit "
-                      "of one round, %.1f s" % (layers, cfg.layers, cfg.name, cfg.batch, cfg.heads, dt)}
+            "sample": "%d layer passes over the %d layers of the %s workload (all %d sequences x %d heads each), "
+                      "verify + commit of one round, %.1f s" % (passes, cfg.layers, cfg.name, cfg.batch,
+                                                                 cfg.heads, dt)}
 
 
 def main():
