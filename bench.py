@@ -52,6 +52,17 @@ def algorithmic_bytes(cfg, pending_len):
     return state + draft + out + factors + pend
 
 
+def graph_plan(steps, layers, max_launches=48):
+    """(steps per captured graph, replays): an even number of steps per graph
+    (the factor stores and inputs ping-pong between consecutive steps), as
+    many as fit in about max_launches kernel launches, dividing the requested
+    step count (rounded up to even) so that exactly that many are timed."""
+    k = steps + (steps % 2)
+    cap = max(2, (max_launches // max(layers, 1)) // 2 * 2)
+    g = max(d for d in range(2, min(cap, k) + 1, 2) if k % d == 0)
+    return g, k // g
+
+
 def cpu_baseline(cfg, rounds, states, budget_s=10.0):
     """The fp64 oracle (verify + commit by definition) on the host cores, on
     whole layers of the same workload, cycling through the layers until about
@@ -93,6 +104,9 @@ def main():
                     help="launch eagerly from Python with HIP events around every launch")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters (if present)")
+    ap.add_argument("--op", default="gdn", choices=["gdn", "conv"],
+                    help="gdn: the recurrent-state verify+commit (the headline); conv: the layer's short "
+                         "causal convolution with its conv-state commit, on the same drafts")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -112,6 +126,8 @@ def main():
     torch.cuda.set_device(dev)
     B.lib()
     cfg = inputs.config(args.workload)
+    if args.op == "conv":
+        return run_conv(args, cfg, torch, B, inputs, dev)
     topo = "chain" if cfg.chain else "tree"
     log("bench: generating %s (%d layers)" % (cfg.name, cfg.layers))
     rnd = inputs.draw_round(cfg, 0)
@@ -172,8 +188,10 @@ def main():
     assert int(status.abs().max()) == 0, "device reported a data error"
 
     if args.graph:
-        # One graph holds two consecutive steps (the factor stores ping-pong),
-        # replayed back to back: no host work between kernel launches.
+        # One graph holds an even number of consecutive steps (the factor
+        # stores ping-pong), replayed back to back: no host work between
+        # kernel launches.
+        gsteps, reps = graph_plan(args.steps, cfg.layers)
         if step_no[0] % 2:
             step()
         g = torch.cuda.CUDAGraph()
@@ -181,14 +199,13 @@ def main():
         s_cap.wait_stream(stream)
         with torch.cuda.stream(s_cap):
             with torch.cuda.graph(g, stream=s_cap):
-                for _ in range(2):
+                for _ in range(gsteps):
                     step()
         torch.cuda.synchronize()
         for _ in range(2):
             g.replay()
         torch.cuda.synchronize()
-        reps = max(1, args.steps // 2)
-        steps = 2 * reps
+        steps = gsteps * reps
         log("bench: timing %d steps (graph replays)" % steps)
         cur = torch.cuda.current_stream(dev)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -244,7 +261,7 @@ def main():
         key = "%s/%s/%s" % (cfg.name, args.route, "separate" if args.separate else "fused")
         # counters taken on other library sources no longer describe this kernel
         from paper_2607_16673_amd.traffic import source_digest
-        if key in tj and tj[key].get("source_sha256") == source_digest():
+        if key in tj and tj[key].get("source_sha256") == source_digest("gdn"):
             traffic = tj[key].get("bytes_per_launch")
             kernel = tj[key].get("kernel")
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -271,6 +288,145 @@ def main():
     if not args.no_cpu_baseline:
         log("bench: oracle CPU baseline")
         line["cpu_baseline"] = cpu_baseline(cfg, rnd, states_np)
+    print(json.dumps(line), flush=True)
+
+
+def conv_algorithmic_bytes(cfg, D, K, pending_len, n_prev):
+    """Bytes one fused conv call must move for one layer: the draft inputs
+    once in, the outputs once out, the conv state once in and once out, the
+    weights, the parent row, and of each pending path only the last K-1
+    accepted rows (plus the path, its parent row and length)."""
+    B, n = cfg.batch, cfg.n_nodes
+    w = 2 if cfg.dtype == "bf16" else 4
+    rows = int(np.sum(np.minimum(pending_len, K - 1)))
+    return (2 * B * n * D * w + 2 * B * (K - 1) * D * 4 + D * K * 4 + B * n * 4
+            + rows * D * w + B * n_prev * 4 * 2 + B * 4)
+
+
+def conv_cpu_baseline(cfg, topo, xs32, Cs, ws, budget_s=10.0):
+    """The fp64 oracle's convolution and conv-state commit on whole layers of
+    the same workload, cycling through the layers for about budget_s."""
+    import oracle
+
+    parent, path, length = topo
+    t0 = time.perf_counter()
+    passes = 0
+    while True:
+        layer = passes % cfg.layers
+        y, st = oracle.conv_verify(Cs[layer], xs32[layer], ws[layer], None, parent)
+        C1, st2 = oracle.conv_commit(Cs[layer], xs32[layer], parent, path, length)
+        assert (st == 0).all() and (st2 == 0).all()
+        passes += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": passes * cfg.batch * cfg.n_nodes / dt, "unit": "nodes/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": "%d layer passes over the %d layers of the %s workload (all %d sequences, %d channels "
+                      "each), convolution + conv-state commit of one round, %.1f s"
+                      % (passes, cfg.layers, cfg.name, cfg.batch, xs32[0].shape[2], dt)}
+
+
+def run_conv(args, cfg, torch, B, inputs, dev):
+    """Timed steps of the short causal convolution: per layer one fused
+    sla_conv_verify with the previous round's accepted rows pending."""
+    D, K = inputs.conv_channels(cfg), inputs.CONV_KERNEL
+    log("bench: generating %s conv inputs (%d layers, %d channels)" % (cfg.name, cfg.layers, D))
+    parent_np, path_np, length_np = inputs.draw_topology(cfg, 0)
+    parent = torch.from_numpy(parent_np).to(dev)
+    path = torch.from_numpy(path_np).to(dev)
+    length = torch.from_numpy(length_np).to(dev)
+
+    def act(x):
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    xs, xs32, Cs, ws = [], [], [], []
+    for l in range(cfg.layers):
+        pair = []
+        for r in range(2):
+            x, x32 = inputs.draw_conv_x(cfg, l, r)
+            pair.append(act(x))
+            if r == 0:
+                xs32.append(x32)
+        xs.append(pair)
+        Cs.append(inputs.draw_conv_state(cfg, l))
+        ws.append(inputs.draw_conv_weight(cfg, l))
+    conv_states = [torch.from_numpy(c).to(dev) for c in Cs]
+    weights = [torch.from_numpy(w).to(dev) for w in ws]
+    ys = [torch.empty_like(xs[l][0]) for l in range(cfg.layers)]
+    status = torch.zeros(cfg.batch, dtype=torch.int32, device=dev)
+    step_no = [0]
+
+    def step():
+        s = step_no[0]
+        for l in range(cfg.layers):
+            pend = (xs[l][(s + 1) % 2], parent, path, length) if s > 0 else None
+            B.sla_conv_verify(conv_states[l], xs[l][s % 2], weights[l], parent, ys[l], pending=pend,
+                              status=status)
+        step_no[0] += 1
+
+    log("bench: warmup %d" % args.warmup)
+    for _ in range(max(args.warmup, 2)):
+        step()
+    if step_no[0] % 2:
+        step()
+    torch.cuda.synchronize()
+    assert int(status.abs().max()) == 0, "device reported a data error"
+    gsteps, reps = graph_plan(args.steps, cfg.layers)
+    g = torch.cuda.CUDAGraph()
+    s_cap = torch.cuda.Stream(dev)
+    s_cap.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s_cap):
+        with torch.cuda.graph(g, stream=s_cap):
+            for _ in range(gsteps):
+                step()
+    torch.cuda.synchronize()
+    for _ in range(2):
+        g.replay()
+    torch.cuda.synchronize()
+    steps = gsteps * reps
+    log("bench: timing %d conv steps (graph replays)" % steps)
+    cur = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    e0.record(cur)
+    for _ in range(reps):
+        g.replay()
+    e1.record(cur)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert int(status.abs().max()) == 0, "device reported a data error"
+    v_ms = e0.elapsed_time(e1) / (steps * cfg.layers)
+    bytes_launch = conv_algorithmic_bytes(cfg, D, K, length_np, cfg.n_nodes)
+    achieved = bytes_launch / (v_ms * 1e-3) / 1e9
+    topo = "chain" if cfg.chain else "tree"
+    line = {
+        "metric": METRIC, "value": round(cfg.batch * cfg.n_nodes * cfg.layers * steps / elapsed, 1),
+        "unit": "nodes/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * elapsed / steps, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "op": "short causal conv (K=%d, SiLU) + conv-state commit" % K,
+                   "batch": cfg.batch, "channels": D, "nodes_per_tree": cfg.n_nodes, "topology": topo,
+                   "layers": cfg.layers, "x_dtype": cfg.dtype, "conv_state_dtype": "f32", "commit": "fused",
+                   "parallelism": "single-gpu", "launch": "hip graph"},
+        "hbm_gbps": round(achieved, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "conv_verify_kernel",
+                     "algorithmic_bytes_per_launch": int(bytes_launch), "avg_launch_ms": round(v_ms, 5)},
+    }
+    if os.path.exists(args.traffic_json):
+        with open(args.traffic_json) as f:
+            tj = json.load(f)
+        key = "%s/conv/fused" % cfg.name
+        from paper_2607_16673_amd.traffic import source_digest
+        if key in tj and tj[key].get("source_sha256") == source_digest("conv"):
+            line["roofline"]["traffic"] = tj[key].get("bytes_per_launch")
+    if not args.no_cpu_baseline:
+        log("bench: oracle CPU baseline (conv)")
+        line["cpu_baseline"] = conv_cpu_baseline(cfg, (parent_np, path_np, length_np), xs32, Cs, ws)
     print(json.dumps(line), flush=True)
 
 

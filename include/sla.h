@@ -174,6 +174,89 @@ int sla_topology(const int32_t *parent_idx, int32_t batch, int32_t n_nodes, int3
                  uint64_t *anc, int32_t *order, int32_t *n_children, int32_t *status,
                  hipStream_t stream);
 
+/* ------------------------------------------------- short causal convolution
+ *
+ * The GDN layer mixes every channel of its q, k and v projections over the
+ * last K tokens with a depthwise causal convolution and SiLU before the
+ * recurrent core, and keeps the last K - 1 committed inputs as a second
+ * per-layer state C next to S (§7: kernel size 4, SiLU, recurrent state
+ * (S, C)).  For channel c,
+ *     y[c] = act(bias[c] + sum_{i=0}^{K-1} w[c][i] z_{K-1-i}[c]),
+ * where z_0 is the node's own input, z_s (s >= 1) the input of its s-th
+ * ancestor on P(j) while one exists, and past the root the committed rows,
+ * newest first: z_s = C[K-2-(s-depth(j))] for s >= depth(j).  So every
+ * node sees only its own root path (tree mask of §4.2), and a chain draft is
+ * an ordinary causal sequence behind C.  act is SiLU, a / (1 + exp(-a)), or
+ * the identity.  Arithmetic is fp32 (fused multiply-adds over i = 0..K-1,
+ * starting from the bias); y is rounded to the activation dtype.
+ *
+ * Commit (§5.1-5.2): accepting a_1..a_A drops the oldest rows of C and
+ * appends x_{a_1}..x_{a_A}: C keeps the last K - 1 rows of
+ * [C[0], .., C[K-2], x_{a_1}, .., x_{a_A}].  The rows are copies (exact:
+ * bf16 and fp32 inputs are held in fp32).  The pre-convolution inputs of
+ * the draft are the conv's factor records: the caller keeps the previous
+ * round's x until the next call has committed from it. */
+
+#define SLA_ACT_NONE 0
+#define SLA_ACT_SILU 1
+#define SLA_CONV_MAX_KERNEL 4
+
+typedef struct sla_conv_shape {
+  int32_t batch;       /* B >= 1                                            */
+  int32_t channels;    /* D, a multiple of 8, 8..(1 << 20)                  */
+  int32_t kernel_size; /* K, 1..SLA_CONV_MAX_KERNEL                         */
+  int32_t n_nodes;     /* draft nodes per sequence, 1..SLA_MAX_NODES        */
+  int32_t x_dtype;     /* SLA_DTYPE_F32 or SLA_DTYPE_BF16 (x and y)         */
+  int32_t activation;  /* SLA_ACT_NONE or SLA_ACT_SILU                      */
+} sla_conv_shape;
+
+/* Pending accepted rows for the conv state (§5.2, delayed update):
+ *   x        the previous round's pre-convolution inputs, device
+ *            [B][n_nodes][D] in shape->x_dtype (read only here);
+ *   parent   the previous round's parent array, device int32 [B][n_nodes];
+ *   n_nodes  that round's n;
+ *   path,len as in sla_pending: device int32 [B][n_nodes] (-1 padded) and
+ *            [B]; path[b][0..len[b]) must be a root path of parent[b]. */
+typedef struct sla_conv_pending {
+  const void *x;
+  const int32_t *parent;
+  int32_t n_nodes;
+  const int32_t *path;
+  const int32_t *len;
+} sla_conv_pending;
+
+/* sla_conv_verify -- the convolution of every draft node of one layer, for
+ * all sequences; optionally first commit a pending accepted path into the
+ * conv state (fused, as sla_verify does for S).
+ *   conv_state device fp32 [B][K-1][D] (NULL allowed when K = 1).  Read only
+ *              with pending == NULL; otherwise the committed rows are
+ *              written back in place and the draft is convolved behind them.
+ *   pending    NULL or the previous round's inputs and accepted path.  Its x
+ *              must not overlap y (SLA_ERR_ALIAS).
+ *   x          device [B][n][D], shape->x_dtype: the pre-convolution inputs.
+ *   weight     device fp32 [D][K]: weight[c][K-1] multiplies the node's own
+ *              input (the layout of a depthwise conv1d weight [D][1][K]).
+ *   bias       device fp32 [D] or NULL (no bias).
+ *   parent_idx device int32 [B][n]; topological order required.
+ *   y          device [B][n][D], shape->x_dtype.
+ *   status     device int32 [B] or NULL: 0, SLA_ERR_TOPOLOGY or
+ *              SLA_ERR_PATH; such a sequence's conv state is untouched and
+ *              its outputs are unspecified.
+ * Returns SLA_OK once the work is enqueued, or a negative error code. */
+int sla_conv_verify(const sla_conv_shape *shape, float *conv_state, const sla_conv_pending *pending,
+                    const void *x, const float *weight, const float *bias, const int32_t *parent_idx,
+                    void *y, int32_t *status, hipStream_t stream);
+
+/* sla_conv_commit -- immediate conv-state update (§5.2): the accepted rows
+ * of x (the draft verified last, shape->n_nodes nodes, parent array
+ * parent_idx) are shifted into C in place.  path, len and status as in
+ * sla_commit (status: 0 or SLA_ERR_PATH); len[b] = 0 leaves sequence b
+ * untouched.  shape->activation is ignored.  Same result, bit for bit, as
+ * the pending prologue of sla_conv_verify. */
+int sla_conv_commit(const sla_conv_shape *shape, float *conv_state, const void *x,
+                    const int32_t *parent_idx, const int32_t *path, const int32_t *len,
+                    int32_t *status, hipStream_t stream);
+
 /* ------------------------------------------------------------ host helpers */
 
 /* Same table as sla_topology for one host-memory parent array, computed

@@ -54,6 +54,10 @@ def _load():
     lib.oracle_verify.restype = ctypes.c_int
     lib.oracle_commit.argtypes = [ctypes.c_int] * 5 + [_dp] * 5 + [_ip, _ip, ctypes.c_int, _ip, _ip]
     lib.oracle_commit.restype = ctypes.c_int
+    lib.oracle_conv_verify.argtypes = [ctypes.c_int] * 4 + [_dp] * 4 + [ctypes.c_int, _ip, _dp, _ip]
+    lib.oracle_conv_verify.restype = ctypes.c_int
+    lib.oracle_conv_commit.argtypes = [ctypes.c_int] * 4 + [_dp, _dp, _ip, _ip, ctypes.c_int, _ip, _ip]
+    lib.oracle_conv_commit.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -183,3 +187,48 @@ def commit(state, k, v, alpha, beta, parent, path, length):
                       _p(bt, _dp), _p(par, _ip), _p(pa, _ip), pa.shape[1], _p(ln, _ip),
                       _p(status, _ip))
     return S, status
+
+
+def conv_verify(conv_state, x, w, bias, parent, activation=True):
+    """Per-node outputs of the short causal convolution by definition.
+
+    Node j's window is the last K inputs of [conv_state rows, x along P(j)]
+    (the GDN layer's depthwise convolution, §7; tree mask of §4.2).
+    conv_state [B][K-1][D]; x [B][n][D]; w [D][K]; bias [D] or None; parent
+    [B][n].  Returns (y [B][n][D] fp64, status [B])."""
+    lib = _load()
+    x = _f64(x)
+    B, n, D = x.shape
+    w = _f64(w)
+    K = w.shape[1]
+    C = _f64(conv_state).reshape(B, K - 1, D) if K > 1 else np.zeros((B, 1, D))
+    bias_p = _p(_f64(bias), _dp) if bias is not None else None
+    par = _i32(parent).reshape(B, n)
+    y = np.zeros((B, n, D))
+    status = np.zeros(B, np.int32)
+    lib.oracle_conv_verify(B, D, K, n, _p(C, _dp), _p(x, _dp), _p(w, _dp), bias_p, int(bool(activation)),
+                           _p(par, _ip), _p(y, _dp), _p(status, _ip))
+    return y, status
+
+
+def conv_commit(conv_state, x, parent, path, length):
+    """Conv state after decoding the accepted tokens one by one (§5.1-5.2):
+    each token drops the oldest row and appends its input.
+
+    conv_state [B][K-1][D]; x [B][n][D]; path [B][stride] (-1 padded);
+    length [B].  Returns (conv_state', status)."""
+    lib = _load()
+    x = _f64(x)
+    B, n, D = x.shape
+    C = _f64(conv_state).copy()
+    K = C.shape[1] + 1
+    Cp = C if K > 1 else np.zeros((B, 1, D))
+    par = _i32(parent).reshape(B, n)
+    pa = _i32(path).reshape(B, -1)
+    if pa.shape[1] == 0:
+        pa = np.full((B, 1), -1, np.int32)
+    ln = _i32(length).reshape(B)
+    status = np.zeros(B, np.int32)
+    lib.oracle_conv_commit(B, D, K, n, _p(Cp, _dp), _p(x, _dp), _p(par, _ip), _p(pa, _ip), pa.shape[1],
+                           _p(ln, _ip), _p(status, _ip))
+    return (Cp if K > 1 else C), status

@@ -27,6 +27,8 @@
  *   - Commit (§5.1 "state recovery", §5.2): the durable state after
  *     accepting the path a_1..a_A is the state after decoding those tokens
  *     one at a time, starting from the committed state.
+ *   - The short causal convolution in front of the recurrent core and its
+ *     conv state (see the section at the end of this file).
  *   - Topology (§4.2 tree mask, §7 parent array): depth, inclusive
  *     ancestor bit masks, child counts and a DFS pre-order, computed by the
  *     definition (following parent pointers node by node).
@@ -39,6 +41,7 @@
  *   state  [B][H][dk][dv]        q, k [B][n][H][dk]      v, out [B][n][H][dv]
  *   alpha, beta [B][n][H]        parent [B][n]           path [B][path_stride]
  */
+#include <math.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -232,5 +235,88 @@ int oracle_commit(int B, int H, int dk, int dv, int n, double *state,
       }
       free(kH);
     }
+  return bad ? OR_ERR_PATH : OR_OK;
+}
+
+/* ------------------------------------------------------------------------
+ * Short causal convolution (the GDN layer's depthwise convolution of kernel
+ * size K = 4 with SiLU, in front of the recurrent core; §7 and the setup of
+ * §8) and its conv state C, the second per-layer state the cache holder
+ * keeps next to S (§7).
+ *
+ * For channel c the convolution of a token sequence z_1..z_t is
+ *     y_t[c] = act(bias[c] + sum_{i=0}^{K-1} w[c][i] * z_{t-K+1+i}[c]),
+ * act = SiLU, silu(a) = a / (1 + exp(-a)), or the identity.  C holds the
+ * last K-1 committed inputs, C[0] the oldest and C[K-2] the newest.
+ *
+ * Verification (§4, with the tree mask of §4.2): the tokens in front of
+ * draft node j are those of its own root path P(j), and in front of those
+ * the committed inputs.  By definition, per node: form the sequence
+ * [C[0], .., C[K-2], x_{p_1}, .., x_{p_d}] with p_1..p_d = P(j) and take
+ * the convolution at its last position.
+ *
+ * Commit (§5.1-5.2): accepting a_1..a_A, the new conv state is the state
+ * after decoding those tokens one at a time, each step dropping the oldest
+ * row of C and appending the token's input.
+ *
+ * Layouts: conv_state [B][K-1][D], x and y [B][n][D], w [D][K], bias [D]. */
+#define OR_MAX_KERNEL 8
+
+static double oracle_silu(double a) { return a / (1.0 + exp(-a)); }
+
+int oracle_conv_verify(int B, int D, int K, int n, const double *conv_state, const double *x,
+                       const double *w, const double *bias, int activation, const int32_t *parent,
+                       double *y, int32_t *status) {
+  if (B < 1 || D < 1 || K < 1 || K > OR_MAX_KERNEL || n < 1 || n > OR_MAX_NODES) return OR_ERR_SHAPE;
+  int bad = 0;
+  for (int b = 0; b < B; ++b) {
+    int st = oracle_check_parent(parent + (size_t)b * n, n);
+    if (status) status[b] = st;
+    if (st != OR_OK) bad = 1;
+  }
+#pragma omp parallel for schedule(dynamic)
+  for (int b = 0; b < B; ++b) {
+    const int32_t *par = parent + (size_t)b * n;
+    if (oracle_check_parent(par, n) != OR_OK) continue;
+    const double *Cb = conv_state + (size_t)b * (K - 1) * D;
+    int32_t path[OR_MAX_NODES];
+    const double *seq[OR_MAX_KERNEL - 1 + OR_MAX_NODES];
+    for (int j = 0; j < n; ++j) {
+      int d = oracle_root_path(par, n, j, path);
+      int L = 0;
+      for (int r = 0; r < K - 1; ++r) seq[L++] = Cb + (size_t)r * D;
+      for (int t = 0; t < d; ++t) seq[L++] = x + ((size_t)b * n + path[t]) * D;
+      double *yj = y + ((size_t)b * n + j) * D;
+      for (int c = 0; c < D; ++c) {
+        double s = bias ? bias[c] : 0.0;
+        for (int i = 0; i < K; ++i) s += w[(size_t)c * K + i] * seq[L - K + i][c];
+        yj[c] = activation ? oracle_silu(s) : s;
+      }
+    }
+  }
+  return bad ? OR_ERR_TOPOLOGY : OR_OK;
+}
+
+int oracle_conv_commit(int B, int D, int K, int n, double *conv_state, const double *x,
+                       const int32_t *parent, const int32_t *path, int path_stride, const int32_t *len,
+                       int32_t *status) {
+  if (B < 1 || D < 1 || K < 1 || K > OR_MAX_KERNEL || n < 1 || n > OR_MAX_NODES) return OR_ERR_SHAPE;
+  int bad = 0;
+  for (int b = 0; b < B; ++b) {
+    const int32_t *par = parent + (size_t)b * n;
+    int st = oracle_check_parent(par, n);
+    if (st == OR_OK) st = oracle_validate_path(par, n, path + (size_t)b * path_stride, len[b]);
+    if (status) status[b] = st;
+    if (st != OR_OK) {
+      bad = 1;
+      continue;
+    }
+    double *Cb = conv_state + (size_t)b * (K - 1) * D;
+    for (int t = 0; t < len[b]; ++t) {
+      const double *xa = x + ((size_t)b * n + path[(size_t)b * path_stride + t]) * D;
+      for (int r = 0; r + 1 < K - 1; ++r) memcpy(Cb + (size_t)r * D, Cb + (size_t)(r + 1) * D, sizeof(double) * D);
+      if (K > 1) memcpy(Cb + (size_t)(K - 2) * D, xa, sizeof(double) * D);
+    }
+  }
   return bad ? OR_ERR_PATH : OR_OK;
 }

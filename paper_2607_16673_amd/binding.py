@@ -36,6 +36,9 @@ SLA_ROUTE_AUTO = 0
 SLA_ROUTE_SERIAL = 1
 SLA_ROUTE_PARALLEL = 2
 SLA_MAX_NODES = 64
+SLA_ACT_NONE = 0
+SLA_ACT_SILU = 1
+SLA_CONV_MAX_KERNEL = 4
 
 ROUTES = {"auto": SLA_ROUTE_AUTO, "serial": SLA_ROUTE_SERIAL, "parallel": SLA_ROUTE_PARALLEL}
 TOPOLOGIES = {"tree": SLA_TOPO_TREE, "chain": SLA_TOPO_CHAIN}
@@ -55,6 +58,16 @@ class SlaFactors(ctypes.Structure):
 class SlaPending(ctypes.Structure):
     _fields_ = [("f", SlaFactors), ("n_nodes", ctypes.c_int32), ("path", ctypes.c_void_p),
                 ("len", ctypes.c_void_p)]
+
+
+class SlaConvShape(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("channels", ctypes.c_int32), ("kernel_size", ctypes.c_int32),
+                ("n_nodes", ctypes.c_int32), ("x_dtype", ctypes.c_int32), ("activation", ctypes.c_int32)]
+
+
+class SlaConvPending(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("parent", ctypes.c_void_p), ("n_nodes", ctypes.c_int32),
+                ("path", ctypes.c_void_p), ("len", ctypes.c_void_p)]
 
 
 class SlaError(RuntimeError):
@@ -90,6 +103,11 @@ def lib():
         L.sla_status_string.argtypes = [ctypes.c_int]
         L.sla_status_string.restype = ctypes.c_char_p
         L.sla_version.restype = ctypes.c_int
+        L.sla_conv_verify.argtypes = [ctypes.POINTER(SlaConvShape), vp, ctypes.POINTER(SlaConvPending),
+                                      vp, vp, vp, vp, vp, vp, vp]
+        L.sla_conv_verify.restype = ctypes.c_int
+        L.sla_conv_commit.argtypes = [ctypes.POINTER(SlaConvShape), vp, vp, vp, vp, vp, vp, vp]
+        L.sla_conv_commit.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -256,3 +274,60 @@ def sla_topology(parent_idx):
                               _dev(status, None, None, "status"), _stream(dev))
     _check(code, "sla_topology")
     return dict(depth=depth, anc=anc, order=order, n_children=kids, status=status)
+
+
+# ------------------------------------------------- short causal convolution
+def make_conv_shape(batch, channels, kernel_size, n_nodes, dtype="bf16", activation=True) -> SlaConvShape:
+    return SlaConvShape(int(batch), int(channels), int(kernel_size), int(n_nodes),
+                        SLA_DTYPE_BF16 if dtype == "bf16" else SLA_DTYPE_F32,
+                        SLA_ACT_SILU if activation else SLA_ACT_NONE)
+
+
+def sla_conv_verify(conv_state, x, weight, parent_idx, y, *, bias=None, pending: Optional[tuple] = None,
+                    status=None, activation: bool = True):
+    """Enqueue the draft's short causal convolution on the current stream
+    (see sla_conv_verify in sla.h).
+
+    conv_state [B][K-1][D] fp32 (None when K = 1); x, y [B][n][D]; weight
+    [D][K] fp32; bias [D] fp32 or None; parent_idx [B][n] int32.
+    pending: None or (x_prev [B][n_prev][D], parent_prev [B][n_prev], path
+    [B][n_prev] int32, len [B] int32).  Raises SlaError on a host-detected error."""
+    torch = _torch()
+    B, n, D = x.shape
+    K = weight.shape[1]
+    shape = make_conv_shape(B, D, K, n, "bf16" if x.dtype == torch.bfloat16 else "f32", activation)
+    _dtype_code(x)
+    cs = _dev(conv_state, torch.float32, (B, K - 1, D), "conv_state") if conv_state is not None else None
+    pend_p = None
+    if pending is not None:
+        px, ppar, ppath, plen = pending
+        pn = ppar.shape[1]
+        pend = SlaConvPending(_dev(px, x.dtype, (B, pn, D), "pending.x"),
+                              _dev(ppar, torch.int32, (B, pn), "pending.parent"), pn,
+                              _dev(ppath, torch.int32, (B, pn), "pending.path"),
+                              _dev(plen, torch.int32, (B,), "pending.len"))
+        pend_p = ctypes.byref(pend)
+    bias_p = _dev(bias, torch.float32, (D,), "bias") if bias is not None else None
+    st_p = _dev(status, torch.int32, (B,), "status") if status is not None else None
+    code = lib().sla_conv_verify(ctypes.byref(shape), cs, pend_p, _dev(x, x.dtype, (B, n, D), "x"),
+                                 _dev(weight, torch.float32, (D, K), "weight"), bias_p,
+                                 _dev(parent_idx, torch.int32, (B, n), "parent_idx"),
+                                 _dev(y, x.dtype, (B, n, D), "y"), st_p, _stream(x.device))
+    _check(code, "sla_conv_verify")
+
+
+def sla_conv_commit(conv_state, x, parent_idx, path, length, *, kernel_size=None, status=None):
+    """Enqueue an immediate conv-state commit of the accepted paths (see
+    sla_conv_commit).  conv_state [B][K-1][D] fp32 (None when K = 1)."""
+    torch = _torch()
+    B, n, D = x.shape
+    K = kernel_size if kernel_size is not None else conv_state.shape[1] + 1
+    shape = make_conv_shape(B, D, K, n, "bf16" if x.dtype == torch.bfloat16 else "f32")
+    _dtype_code(x)
+    cs = _dev(conv_state, torch.float32, (B, K - 1, D), "conv_state") if conv_state is not None else None
+    st_p = _dev(status, torch.int32, (B,), "status") if status is not None else None
+    code = lib().sla_conv_commit(ctypes.byref(shape), cs, _dev(x, x.dtype, (B, n, D), "x"),
+                                 _dev(parent_idx, torch.int32, (B, n), "parent_idx"),
+                                 _dev(path, torch.int32, (B, n), "path"),
+                                 _dev(length, torch.int32, (B,), "len"), st_p, _stream(x.device))
+    _check(code, "sla_conv_commit")

@@ -57,6 +57,17 @@ bool factors_complete(const sla_factors *f) { return f && f->k && f->u && f->alp
 
 int hip_status(hipError_t e) { return e == hipSuccess ? SLA_OK : SLA_ERR_HIP; }
 
+int check_conv_shape(const sla_conv_shape *s) {
+  if (!s) return SLA_ERR_NULL;
+  if (s->batch < 1 || s->n_nodes < 1 || s->n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+  if (s->channels < 8 || s->channels % 8 != 0 || s->channels > (1 << 20)) return SLA_ERR_SHAPE;
+  if (s->kernel_size < 1 || s->kernel_size > SLA_CONV_MAX_KERNEL) return SLA_ERR_SHAPE;
+  if (s->x_dtype != SLA_DTYPE_F32 && s->x_dtype != SLA_DTYPE_BF16) return SLA_ERR_DTYPE;
+  if (s->activation != SLA_ACT_NONE && s->activation != SLA_ACT_SILU) return SLA_ERR_SHAPE;
+  if ((uint64_t)s->batch * (uint64_t)((s->channels + 511) / 512) > (1ull << 30)) return SLA_ERR_SHAPE;
+  return SLA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -183,6 +194,71 @@ int sla_commit(const sla_shape *shape, float *state, const sla_factors *factors,
   a.len = len;
   a.status = status;
   return hip_status(sla::launch_commit(a, shape->qkv_dtype, stream));
+}
+
+int sla_conv_verify(const sla_conv_shape *shape, float *conv_state, const sla_conv_pending *pending,
+                    const void *x, const float *weight, const float *bias, const int32_t *parent_idx, void *y,
+                    int32_t *status, hipStream_t stream) {
+  int st = check_conv_shape(shape);
+  if (st != SLA_OK) return st;
+  const int K = shape->kernel_size;
+  if (!x || !weight || !parent_idx || !y || (K > 1 && !conv_state)) return SLA_ERR_NULL;
+  const size_t w = act_bytes(shape->x_dtype);
+  if (pending) {
+    if (!pending->x || !pending->parent || !pending->path || !pending->len) return SLA_ERR_NULL;
+    if (pending->n_nodes < 1 || pending->n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+    const size_t out_bytes = (size_t)shape->batch * shape->n_nodes * shape->channels * w;
+    const size_t in_bytes = (size_t)shape->batch * pending->n_nodes * shape->channels * w;
+    if (overlaps(range_of(y, out_bytes), range_of(pending->x, in_bytes))) return SLA_ERR_ALIAS;
+    if (!aligned16(pending->x)) return SLA_ERR_UNSUPPORTED;
+  }
+  if (!aligned16(x) || !aligned16(y) || !aligned16(weight) || (K > 1 && !aligned16(conv_state)))
+    return SLA_ERR_UNSUPPORTED;
+  sla::ConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.B = shape->batch;
+  a.D = shape->channels;
+  a.K = K;
+  a.n = shape->n_nodes;
+  a.activation = shape->activation;
+  a.has_pending = pending != nullptr;
+  a.conv_state = conv_state;
+  a.x = x;
+  a.weight = weight;
+  a.bias = bias;
+  a.parent = parent_idx;
+  a.y = y;
+  if (pending) {
+    a.pend_x = pending->x;
+    a.pend_parent = pending->parent;
+    a.pend_n = pending->n_nodes;
+    a.path = pending->path;
+    a.len = pending->len;
+  }
+  a.status = status;
+  return hip_status(sla::launch_conv(a, shape->x_dtype, false, stream));
+}
+
+int sla_conv_commit(const sla_conv_shape *shape, float *conv_state, const void *x, const int32_t *parent_idx,
+                    const int32_t *path, const int32_t *len, int32_t *status, hipStream_t stream) {
+  int st = check_conv_shape(shape);
+  if (st != SLA_OK) return st;
+  const int K = shape->kernel_size;
+  if (!x || !parent_idx || !path || !len || (K > 1 && !conv_state)) return SLA_ERR_NULL;
+  if (!aligned16(x) || (K > 1 && !aligned16(conv_state))) return SLA_ERR_UNSUPPORTED;
+  sla::ConvArgs a;
+  memset(&a, 0, sizeof(a));
+  a.B = shape->batch;
+  a.D = shape->channels;
+  a.K = K;
+  a.n = shape->n_nodes;
+  a.conv_state = conv_state;
+  a.x = x;
+  a.parent = parent_idx;
+  a.path = path;
+  a.len = len;
+  a.status = status;
+  return hip_status(sla::launch_conv(a, shape->x_dtype, true, stream));
 }
 
 int sla_topology(const int32_t *parent_idx, int32_t batch, int32_t n_nodes, int32_t *depth, uint64_t *anc,

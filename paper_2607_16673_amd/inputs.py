@@ -16,7 +16,13 @@ proposal trees of the paper's evaluation, §8, which are not available):
     uniform parent among earlier nodes whose depth and child count are still
     below the configured limits;
   * accepted path: chains accept a uniform prefix length in [0, n]; trees
-    accept the root path of a uniformly drawn node.
+    accept the root path of a uniformly drawn node;
+  * short convolution in front of the recurrent core: its channels are the
+    q, k and v projections of all heads, D = H (2 d_k + d_v); pre-convolution
+    inputs x ~ N(0, 1) rounded to the activation dtype; committed conv state
+    (earlier inputs) drawn the same way and held in fp32; depthwise weights
+    [D][K] ~ U(-1/sqrt(K), 1/sqrt(K)) in fp32 (the default initialisation of a
+    depthwise conv1d), kernel size K = 4, no bias.
 """
 from __future__ import annotations
 
@@ -213,3 +219,41 @@ def draw_round(cfg: Config, round_index: int = 0, layers=None, batch: int | None
         r.q32.append(d["q32"]); r.k32.append(d["k32"]); r.v32.append(d["v32"])
         r.alpha.append(d["alpha"]); r.beta.append(d["beta"])
     return r
+
+
+# ---------------------------------------------------------------- short convolution
+CONV_KERNEL = 4
+
+
+def conv_channels(cfg: Config) -> int:
+    """Channels of the layer's short convolution: q, k and v of every head."""
+    return cfg.heads * (2 * cfg.d_k + cfg.d_v)
+
+
+def draw_conv_x(cfg: Config, layer: int, round_index: int = 0, batch: int | None = None,
+                channels: int | None = None):
+    """Pre-convolution inputs of one layer of one round, [B][n][D]:
+    (storage array, exact fp32 values)."""
+    B = cfg.batch if batch is None else batch
+    D = conv_channels(cfg) if channels is None else channels
+    rng = _rng(base_seed(cfg), round_index, 3, layer)
+    return _to_dtype(rng.standard_normal((B, cfg.n_nodes, D), dtype=np.float32), cfg.dtype)
+
+
+def draw_conv_weight(cfg: Config, layer: int, channels: int | None = None, kernel: int = CONV_KERNEL) -> np.ndarray:
+    """Depthwise weights [D][K], fp32."""
+    D = conv_channels(cfg) if channels is None else channels
+    rng = _rng(base_seed(cfg), 4, layer)
+    lim = 1.0 / np.sqrt(kernel)
+    return rng.uniform(-lim, lim, (D, kernel)).astype(np.float32)
+
+
+def draw_conv_state(cfg: Config, layer: int, batch: int | None = None, channels: int | None = None,
+                    kernel: int = CONV_KERNEL) -> np.ndarray:
+    """Committed conv state [B][K-1][D]: earlier inputs (activation-dtype
+    values) held in fp32."""
+    B = cfg.batch if batch is None else batch
+    D = conv_channels(cfg) if channels is None else channels
+    rng = _rng(base_seed(cfg), 5, layer)
+    _, c32 = _to_dtype(rng.standard_normal((B, kernel - 1, D), dtype=np.float32), cfg.dtype)
+    return np.ascontiguousarray(c32)

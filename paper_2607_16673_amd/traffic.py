@@ -38,10 +38,18 @@ KERNEL_TAG = "verify_tile_kernel"
 COPY_TAG = "mul"  # the elementwise multiply of run_copy (not the fill before it)
 
 
-def source_digest() -> str:
-    """sha256 over the library sources: counters taken on other sources are stale."""
+# the sources each counted kernel is built from: counters taken on other
+# sources are stale
+SOURCES = {
+    "gdn": ["verify_tile.hip", "verify_serial.hip", "commit.hip", "device.hpp", "kernels.hpp"],
+    "conv": ["conv.hip", "device.hpp", "kernels.hpp"],
+}
+
+
+def source_digest(op: str = "gdn") -> str:
+    """sha256 over the sources of the kernels of one op (gdn or conv)."""
     h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(HERE, "csrc", "*"))) + [os.path.join(ROOT, "include", "sla.h")]
+    files = [os.path.join(HERE, "csrc", f) for f in SOURCES[op]]
     for fn in files:
         with open(fn, "rb") as f:
             h.update(os.path.basename(fn).encode() + b"\0" + f.read())
@@ -97,26 +105,27 @@ def _per_dispatch_kib(rows, tag, skip=0):
     return sum(vals) / len(vals), len(vals)
 
 
-def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, json_path: str) -> dict:
+def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, json_path: str,
+              kernel: str = KERNEL_TAG) -> dict:
     copy_bytes = COPY_MIB * (1 << 20)  # per copy dispatch, read and written
     cf, _ = _per_dispatch_kib(_rows(os.path.join(out_dir, "copy_fetch"), "FETCH_SIZE"), COPY_TAG, 0)
     cw, _ = _per_dispatch_kib(_rows(os.path.join(out_dir, "copy_write"), "WRITE_SIZE"), COPY_TAG, 0)
     scale_f = copy_bytes / (cf * 1024.0)
     scale_w = copy_bytes / (cw * 1024.0)
-    bf, nf = _per_dispatch_kib(_rows(os.path.join(out_dir, "bench_fetch"), "FETCH_SIZE"), KERNEL_TAG, skip)
-    bw, nw = _per_dispatch_kib(_rows(os.path.join(out_dir, "bench_write"), "WRITE_SIZE"), KERNEL_TAG, skip)
+    bf, nf = _per_dispatch_kib(_rows(os.path.join(out_dir, "bench_fetch"), "FETCH_SIZE"), kernel, skip)
+    bw, nw = _per_dispatch_kib(_rows(os.path.join(out_dir, "bench_write"), "WRITE_SIZE"), kernel, skip)
     fetch = bf * 1024.0 * scale_f
     write = bw * 1024.0 * scale_w
     key = "%s/%s/%s" % (workload, route, mode)
     entry = {
-        "kernel": KERNEL_TAG,
+        "kernel": kernel,
         "bytes_per_launch": int(round(fetch + write)),
         "fetch_bytes_per_launch": int(round(fetch)),
         "write_bytes_per_launch": int(round(write)),
         "fetch_kib_raw": round(bf, 1), "write_kib_raw": round(bw, 1),
         "copy_scale_fetch": round(scale_f, 4), "copy_scale_write": round(scale_w, 4),
         "dispatches": [nf, nw],
-        "source_sha256": source_digest(),
+        "source_sha256": source_digest("conv" if route == "conv" else "gdn"),
     }
     data = {}
     if os.path.exists(json_path):
@@ -137,7 +146,8 @@ def main(argv=None) -> None:
     s = sub.add_parser("summarize")
     s.add_argument("--out-dir", required=True)
     s.add_argument("--workload", required=True)
-    s.add_argument("--route", default="auto")
+    s.add_argument("--route", default="auto", help="auto, serial, parallel, or conv for the convolution")
+    s.add_argument("--kernel", default=KERNEL_TAG, help="kernel name substring to average")
     s.add_argument("--mode", default="fused")
     s.add_argument("--skip", type=int, default=0,
                    help="leading verify dispatches to ignore (the first step has no pending path)")
@@ -146,7 +156,7 @@ def main(argv=None) -> None:
     if a.cmd == "copy":
         run_copy(a.mib)
     else:
-        print(json.dumps(summarize(a.out_dir, a.workload, a.route, a.mode, a.skip, a.json), indent=1))
+        print(json.dumps(summarize(a.out_dir, a.workload, a.route, a.mode, a.skip, a.json, a.kernel), indent=1))
 
 
 if __name__ == "__main__":

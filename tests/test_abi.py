@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     syms = declared_symbols()
     assert {"sla_verify", "sla_commit", "sla_topology", "sla_topology_host",
             "sla_validate_path_host", "sla_factors_bytes", "sla_status_string",
-            "sla_version"} <= set(syms)
+            "sla_version", "sla_conv_verify", "sla_conv_commit"} <= set(syms)
     for s in syms:
         assert hasattr(L, s), s
 
@@ -187,3 +187,51 @@ def test_binding_refuses_host_tensors():
         B.sla_verify(torch.zeros(1, 1, 64, 64), x, x, x, torch.zeros(1, 4, 1), torch.zeros(1, 4, 1),
                      torch.zeros(1, 4, dtype=torch.int32), torch.zeros(1, 4, 1, 64),
                      B.Factors(x, x, torch.zeros(1, 4, 1), torch.zeros(1, 4, dtype=torch.int32)))
+
+
+def _conv_verify(shape, pending=None, nulls=(), cs=None, x=None, y=None):
+    args = [_ptr(i) for i in range(6)]
+    for i in nulls:
+        args[i] = None
+    return B.lib().sla_conv_verify(ctypes.byref(shape) if shape is not None else None,
+                                   cs if cs is not None else args[0],
+                                   ctypes.byref(pending) if pending is not None else None,
+                                   x if x is not None else args[1], args[2], args[3], args[4],
+                                   y if y is not None else args[5], None, None)
+
+
+def test_conv_argument_errors_return_before_launch():
+    L = B.lib()
+    ok = B.make_conv_shape(4, 6144, 4, 16)
+    assert _conv_verify(None) == B.SLA_ERR_NULL
+    for i in [0, 1, 2, 4, 5]:  # conv_state, x, weight, parent, y (bias may be NULL)
+        assert _conv_verify(ok, nulls=(i,)) == B.SLA_ERR_NULL, i
+    # with K = 1 there is no conv state, so a NULL one is fine (fails later on alignment)
+    k1 = B.make_conv_shape(4, 6144, 1, 16)
+    assert _conv_verify(k1, nulls=(0,), x=ctypes.c_void_p(FAKE + 8)) == B.SLA_ERR_UNSUPPORTED
+    for s in [B.make_conv_shape(0, 64, 4, 16), B.make_conv_shape(4, 60, 4, 16), B.make_conv_shape(4, 0, 4, 16),
+              B.make_conv_shape(4, 64, 0, 16), B.make_conv_shape(4, 64, 5, 16), B.make_conv_shape(4, 64, 4, 0),
+              B.make_conv_shape(4, 64, 4, 65), B.make_conv_shape(4, (1 << 20) + 8, 4, 16)]:
+        assert _conv_verify(s) == B.SLA_ERR_SHAPE
+    s = B.make_conv_shape(4, 64, 4, 16)
+    s.x_dtype = 5
+    assert _conv_verify(s) == B.SLA_ERR_DTYPE
+    s = B.make_conv_shape(4, 64, 4, 16)
+    s.activation = 2
+    assert _conv_verify(s) == B.SLA_ERR_SHAPE
+    # pending rows overlapping the outputs, incomplete or mis-sized pending
+    y = _ptr(5)
+    alias = B.SlaConvPending(ctypes.c_void_p(FAKE + 5 * (1 << 24) + 1024), _ptr(7), 16, _ptr(8), _ptr(9))
+    assert _conv_verify(ok, pending=alias, y=y) == B.SLA_ERR_ALIAS
+    assert _conv_verify(ok, pending=B.SlaConvPending(_ptr(6), None, 16, _ptr(8), _ptr(9))) == B.SLA_ERR_NULL
+    assert _conv_verify(ok, pending=B.SlaConvPending(_ptr(6), _ptr(7), 0, _ptr(8), _ptr(9))) == B.SLA_ERR_SHAPE
+    assert _conv_verify(ok, x=ctypes.c_void_p(FAKE + 8)) == B.SLA_ERR_UNSUPPORTED
+    # standalone commit
+    c = L.sla_conv_commit
+    assert c(None, _ptr(0), _ptr(1), _ptr(2), _ptr(3), _ptr(4), None, None) == B.SLA_ERR_NULL
+    for i in range(5):
+        args = [_ptr(j) for j in range(5)]
+        args[i] = None
+        assert c(ctypes.byref(ok), *args, None, None) == B.SLA_ERR_NULL, i
+    assert c(ctypes.byref(B.make_conv_shape(4, 64, 4, 70)), *[_ptr(j) for j in range(5)], None, None) == \
+        B.SLA_ERR_SHAPE
