@@ -104,9 +104,10 @@ def main():
                     help="launch eagerly from Python with HIP events around every launch")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters (if present)")
-    ap.add_argument("--op", default="gdn", choices=["gdn", "conv"],
+    ap.add_argument("--op", default="gdn", choices=["gdn", "conv", "prune"],
                     help="gdn: the recurrent-state verify+commit (the headline); conv: the layer's short "
-                         "causal convolution with its conv-state commit, on the same drafts")
+                         "causal convolution with its conv-state commit, on the same drafts; prune: draft "
+                         "pruning and packing of 64-candidate rollouts down to the workload's tree size")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -128,6 +129,8 @@ def main():
     cfg = inputs.config(args.workload)
     if args.op == "conv":
         return run_conv(args, cfg, torch, B, inputs, dev)
+    if args.op == "prune":
+        return run_prune(args, cfg, torch, B, inputs, dev)
     topo = "chain" if cfg.chain else "tree"
     log("bench: generating %s (%d layers)" % (cfg.name, cfg.layers))
     rnd = inputs.draw_round(cfg, 0)
@@ -427,6 +430,76 @@ def run_conv(args, cfg, torch, B, inputs, dev):
     if not args.no_cpu_baseline:
         log("bench: oracle CPU baseline (conv)")
         line["cpu_baseline"] = conv_cpu_baseline(cfg, (parent_np, path_np, length_np), xs32, Cs, ws)
+    print(json.dumps(line), flush=True)
+
+
+def run_prune(args, cfg, torch, B, inputs, dev, n_cand=64, tau=3.0):
+    """Timed steps of draft pruning and packing: per step (one speculative
+    round) one sla_prune over every sequence's 64-candidate rollout, margin
+    tau and the workload's tree size as the budget."""
+    T = cfg.n_nodes
+    par_np, lp_np = inputs.draw_rollouts(cfg, 0, n_cand=n_cand)
+    par = torch.from_numpy(par_np).to(dev)
+    lp = torch.from_numpy(lp_np).to(dev)
+    out = {}
+
+    def step():
+        out.update(B.sla_prune(par, lp, tau, T))
+
+    for _ in range(max(args.warmup, 2)):
+        step()
+    torch.cuda.synchronize()
+    assert int(out["status"].abs().max()) == 0
+    gsteps, reps = graph_plan(args.steps, 1)
+    g = torch.cuda.CUDAGraph()
+    s_cap = torch.cuda.Stream(dev)
+    s_cap.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s_cap):
+        with torch.cuda.graph(g, stream=s_cap):
+            for _ in range(gsteps):
+                step()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    steps = gsteps * reps
+    cur = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(cur)
+    for _ in range(reps):
+        g.replay()
+    e1.record(cur)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    v_ms = e0.elapsed_time(e1) / steps
+    kept = float(out["count"].float().mean())
+    bytes_launch = cfg.batch * n_cand * (4 + 4 + 4 + 4) + cfg.batch * 8
+    achieved = bytes_launch / (v_ms * 1e-3) / 1e9
+    line = {
+        "metric": "pruned draft sequences/sec", "value": round(cfg.batch * steps / elapsed, 1),
+        "unit": "sequences/s", "n_gpus": 1, "steps": steps, "warmup": args.warmup,
+        "ms_per_step": round(1e3 * elapsed / steps, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "op": "draft pruning + packing", "batch": cfg.batch,
+                   "candidates": n_cand, "rollout": "beam top-4", "tau": tau, "budget": T,
+                   "mean_kept": round(kept, 2), "parallelism": "single-gpu", "launch": "hip graph"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 6), "traffic": None, "kernel": "prune_kernel",
+                     "algorithmic_bytes_per_launch": int(bytes_launch), "avg_launch_ms": round(v_ms, 5)},
+    }
+    if not args.no_cpu_baseline:
+        from oracle import prune as P
+        t0 = time.perf_counter()
+        done = 0
+        while time.perf_counter() - t0 < 10.0:
+            b = done % cfg.batch
+            keep, q, st = P.prune(par_np[b], lp_np[b], tau, T)
+            P.pack(par_np[b], keep)
+            done += 1
+        dt = time.perf_counter() - t0
+        line["cpu_baseline"] = {"value": round(done / dt, 1), "unit": "sequences/s", "cores": 1, "kind": "oracle",
+                                "sample": "%d sequences of the rollout set, pruned and packed one by one, %.1f s"
+                                          % (done, dt)}
     print(json.dumps(line), flush=True)
 
 

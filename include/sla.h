@@ -54,6 +54,7 @@ extern "C" {
 #define SLA_ERR_ALIAS (-6)       /* pending factors overlap output factors */
 #define SLA_ERR_UNSUPPORTED (-7) /* valid request this build cannot run    */
 #define SLA_ERR_HIP (-8)         /* the HIP runtime reported an error      */
+#define SLA_ERR_SCORE (-9)       /* a draft log-probability above 0 or NaN */
 
 /* Activation dtypes of q, k, v (and of the stored k factor). */
 #define SLA_DTYPE_F32 0
@@ -256,6 +257,57 @@ int sla_conv_verify(const sla_conv_shape *shape, float *conv_state, const sla_co
 int sla_conv_commit(const sla_conv_shape *shape, float *conv_state, const void *x,
                     const int32_t *parent_idx, const int32_t *path, const int32_t *len,
                     int32_t *status, hipStream_t stream);
+
+/* ------------------------------------------ draft pruning and packing (§6.1)
+ *
+ * After the drafter's rollout every candidate v has a parent (-1: a child of
+ * the committed state; parent[v] < v) and the log-probability logp[v] <= 0 of
+ * its token given its path.  Its score is the path's joint log-probability,
+ * summed root first in fp32: q(v) = q(parent(v)) + logp(v).  With q* the best
+ * score and margin tau, the window keeps q(v) >= q* - tau (§6.1, "Tree
+ * pruning"; the threshold q* - tau is an fp32 value).  A budget T > 0 then
+ * keeps the first T window nodes in (score descending, index ascending)
+ * order: since scores never increase along a path and parents carry smaller
+ * indices, every ancestor ranks ahead of its descendants, so the kept set is
+ * ancestor-closed -- what taking candidates in score order together with
+ * their missing ancestors until T is used up selects.  Packing renumbers the
+ * kept nodes 0..m-1 in their original (topological) order: packed_parent is
+ * the verifier's parent array (§7), index_map[new] = old gathers the kept
+ * tokens and activations.  Rows m..n-1 of both are -1. */
+
+/* sla_prune -- batched on the device, one sequence per wavefront.
+ *   parent, logp   device int32 / fp32 [B][n], n <= SLA_MAX_NODES;
+ *   tau            margin (>= 0); budget T, <= 0 for none;
+ *   packed_parent, index_map  device int32 [B][n] (written);
+ *   count          device int32 [B]: kept nodes m (0 on a data error);
+ *   scores         device fp32 [B][n] or NULL: q(v);
+ *   status         device int32 [B] or NULL: 0, SLA_ERR_TOPOLOGY or
+ *                  SLA_ERR_SCORE (then the rows are unspecified). */
+int sla_prune(const int32_t *parent, const float *logp, int32_t batch, int32_t n_nodes, float tau,
+              int32_t budget, int32_t *packed_parent, int32_t *index_map, int32_t *count, float *scores,
+              int32_t *status, hipStream_t stream);
+
+/* sla_prune_host -- the same for one host-memory sequence, synchronously on
+ * the CPU, for any n in 1..65536.  Returns SLA_OK, SLA_ERR_NULL,
+ * SLA_ERR_SHAPE, SLA_ERR_TOPOLOGY or SLA_ERR_SCORE; *count = m. */
+int sla_prune_host(const int32_t *parent, const float *logp, int32_t n_nodes, float tau, int32_t budget,
+                   int32_t *packed_parent, int32_t *index_map, int32_t *count, float *scores);
+
+/* Tree mask -> parent array (§7, the proposal converter; the mask is M_tree
+ * of §4.2).  mask[b][i] is row i as a bit set: bit j is set iff node j is an
+ * ancestor of node i or i itself (n <= 64).  The parent of i is its deepest
+ * strict ancestor, which in topological order is the one with the highest
+ * index.  A mask that is not a tree mask in topological order (a missing
+ * diagonal bit, an ancestor after its descendant, ancestors that do not form
+ * one chain) is SLA_ERR_TOPOLOGY.
+ *   sla_tree_mask_to_parent: device mask uint64 [B][n], parent int32 [B][n],
+ *   status int32 [B] or NULL (on an error that row's parents are not written). */
+int sla_tree_mask_to_parent(const uint64_t *mask, int32_t batch, int32_t n_nodes, int32_t *parent,
+                            int32_t *status, hipStream_t stream);
+
+/* Host version for one mask: returns SLA_OK, SLA_ERR_NULL, SLA_ERR_SHAPE or
+ * SLA_ERR_TOPOLOGY. */
+int sla_tree_mask_to_parent_host(const uint64_t *mask, int32_t n_nodes, int32_t *parent);
 
 /* ------------------------------------------------------------ host helpers */
 

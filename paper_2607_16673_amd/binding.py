@@ -27,6 +27,7 @@ SLA_ERR_PATH = -5
 SLA_ERR_ALIAS = -6
 SLA_ERR_UNSUPPORTED = -7
 SLA_ERR_HIP = -8
+SLA_ERR_SCORE = -9
 
 SLA_DTYPE_F32 = 0
 SLA_DTYPE_BF16 = 1
@@ -108,6 +109,14 @@ def lib():
         L.sla_conv_verify.restype = ctypes.c_int
         L.sla_conv_commit.argtypes = [ctypes.POINTER(SlaConvShape), vp, vp, vp, vp, vp, vp, vp]
         L.sla_conv_commit.restype = ctypes.c_int
+        L.sla_prune.argtypes = [vp, vp, i32, i32, ctypes.c_float, i32, vp, vp, vp, vp, vp, vp]
+        L.sla_prune.restype = ctypes.c_int
+        L.sla_prune_host.argtypes = [vp, vp, i32, ctypes.c_float, i32, vp, vp, vp, vp]
+        L.sla_prune_host.restype = ctypes.c_int
+        L.sla_tree_mask_to_parent.argtypes = [vp, i32, i32, vp, vp, vp]
+        L.sla_tree_mask_to_parent.restype = ctypes.c_int
+        L.sla_tree_mask_to_parent_host.argtypes = [vp, i32, vp]
+        L.sla_tree_mask_to_parent_host.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -331,3 +340,68 @@ def sla_conv_commit(conv_state, x, parent_idx, path, length, *, kernel_size=None
                                  _dev(path, torch.int32, (B, n), "path"),
                                  _dev(length, torch.int32, (B,), "len"), st_p, _stream(x.device))
     _check(code, "sla_conv_commit")
+
+
+# ------------------------------------------------- draft pruning and packing
+def sla_prune_host(parent, logp, tau: float, budget: int = 0) -> dict:
+    """Prune and pack one draft on the CPU (see sla_prune_host in sla.h).
+    Returns dict(status, count, packed_parent, index_map, scores)."""
+    p = np.ascontiguousarray(np.asarray(parent, dtype=np.int32))
+    lp = np.ascontiguousarray(np.asarray(logp, dtype=np.float32))
+    n = len(p)
+    pp = np.zeros(max(n, 1), np.int32)
+    im = np.zeros(max(n, 1), np.int32)
+    sc = np.zeros(max(n, 1), np.float32)
+    cnt = np.zeros(1, np.int32)
+    st = lib().sla_prune_host(p.ctypes.data, lp.ctypes.data, n, float(tau), int(budget), pp.ctypes.data,
+                              im.ctypes.data, cnt.ctypes.data, sc.ctypes.data)
+    return dict(status=st, count=int(cnt[0]), packed_parent=pp[:n], index_map=im[:n], scores=sc[:n])
+
+
+def sla_prune(parent, logp, tau: float, budget: int = 0, *, with_scores: bool = False):
+    """Enqueue batched pruning and packing on the current stream (see
+    sla_prune).  parent [B][n] int32, logp [B][n] fp32 (device tensors).
+    Returns dict of device tensors: packed_parent, index_map, count, status
+    (and scores)."""
+    torch = _torch()
+    B, n = parent.shape
+    dev = parent.device
+    pp = torch.empty(B, n, dtype=torch.int32, device=dev)
+    im = torch.empty(B, n, dtype=torch.int32, device=dev)
+    cnt = torch.empty(B, dtype=torch.int32, device=dev)
+    st = torch.empty(B, dtype=torch.int32, device=dev)
+    sc = torch.empty(B, n, dtype=torch.float32, device=dev) if with_scores else None
+    code = lib().sla_prune(_dev(parent, torch.int32, (B, n), "parent"), _dev(logp, torch.float32, (B, n), "logp"),
+                           B, n, float(tau), int(budget), _dev(pp, None, None, "packed_parent"),
+                           _dev(im, None, None, "index_map"), _dev(cnt, None, None, "count"),
+                           _dev(sc, None, None, "scores") if sc is not None else None,
+                           _dev(st, None, None, "status"), _stream(dev))
+    _check(code, "sla_prune")
+    out = dict(packed_parent=pp, index_map=im, count=cnt, status=st)
+    if sc is not None:
+        out["scores"] = sc
+    return out
+
+
+def sla_tree_mask_to_parent_host(mask_rows):
+    """(status, parent) from one tree mask given as uint64 row bit sets."""
+    m = np.ascontiguousarray(np.asarray(mask_rows, dtype=np.uint64))
+    n = len(m)
+    out = np.zeros(max(n, 1), np.int32)
+    st = lib().sla_tree_mask_to_parent_host(m.ctypes.data, n, out.ctypes.data)
+    return st, out[:n]
+
+
+def sla_tree_mask_to_parent(mask_rows):
+    """Batched device converter: mask_rows [B][n] int64 (uint64 bit sets).
+    Returns (parent [B][n] int32, status [B] int32) device tensors."""
+    torch = _torch()
+    B, n = mask_rows.shape
+    dev = mask_rows.device
+    par = torch.full((B, n), -2, dtype=torch.int32, device=dev)
+    st = torch.empty(B, dtype=torch.int32, device=dev)
+    code = lib().sla_tree_mask_to_parent(_dev(mask_rows, torch.int64, (B, n), "mask"), B, n,
+                                         _dev(par, None, None, "parent"), _dev(st, None, None, "status"),
+                                         _stream(dev))
+    _check(code, "sla_tree_mask_to_parent")
+    return par, st

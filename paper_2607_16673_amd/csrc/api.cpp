@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "kernels.hpp"
@@ -85,6 +86,7 @@ const char *sla_status_string(int status) {
     case SLA_ERR_ALIAS: return "pending factors overlap output factors";
     case SLA_ERR_UNSUPPORTED: return "unsupported configuration";
     case SLA_ERR_HIP: return "HIP runtime error";
+    case SLA_ERR_SCORE: return "draft log-probability above 0 or NaN";
     default: return "unknown status";
   }
 }
@@ -259,6 +261,83 @@ int sla_conv_commit(const sla_conv_shape *shape, float *conv_state, const void *
   a.len = len;
   a.status = status;
   return hip_status(sla::launch_conv(a, shape->x_dtype, true, stream));
+}
+
+int sla_prune(const int32_t *parent, const float *logp, int32_t batch, int32_t n_nodes, float tau, int32_t budget,
+              int32_t *packed_parent, int32_t *index_map, int32_t *count, float *scores, int32_t *status,
+              hipStream_t stream) {
+  if (!parent || !logp || !packed_parent || !index_map || !count) return SLA_ERR_NULL;
+  if (batch < 1 || batch > (1 << 30) || n_nodes < 1 || n_nodes > SLA_MAX_NODES || !(tau >= 0.f)) return SLA_ERR_SHAPE;
+  sla::PruneArgs a{batch, n_nodes, tau, budget, parent, logp, packed_parent, index_map, count, scores, status};
+  return hip_status(sla::launch_prune(a, stream));
+}
+
+// Host pruning: scores root first (parents precede children), the window,
+// the budgeted prefix in (score desc, index asc) order, then packing.
+int sla_prune_host(const int32_t *parent, const float *logp, int32_t n, float tau, int32_t budget,
+                   int32_t *packed_parent, int32_t *index_map, int32_t *count, float *scores) {
+  if (!parent || !logp || !packed_parent || !index_map || !count) return SLA_ERR_NULL;
+  if (n < 1 || n > (1 << 16) || !(tau >= 0.f)) return SLA_ERR_SHAPE;
+  for (int j = 0; j < n; ++j)
+    if (parent[j] < -1 || parent[j] >= j) return SLA_ERR_TOPOLOGY;
+  for (int j = 0; j < n; ++j)
+    if (!(logp[j] <= 0.f)) return SLA_ERR_SCORE;
+  std::vector<float> q(n);
+  for (int j = 0; j < n; ++j) q[j] = parent[j] >= 0 ? q[parent[j]] + logp[j] : logp[j];
+  float qstar = q[0];
+  for (int j = 1; j < n; ++j) qstar = std::max(qstar, q[j]);
+  const float thr = qstar - tau;
+  std::vector<int> window;
+  for (int j = 0; j < n; ++j)
+    if (q[j] >= thr) window.push_back(j);
+  std::vector<char> keep(n, 0);
+  if (budget > 0 && (int)window.size() > budget) {
+    std::stable_sort(window.begin(), window.end(), [&](int x, int y) { return q[x] > q[y]; });
+    for (int i = 0; i < budget; ++i) keep[window[i]] = 1;
+  } else {
+    for (int j : window) keep[j] = 1;
+  }
+  std::vector<int> nidx(n, -1);
+  int m = 0;
+  for (int j = 0; j < n; ++j)
+    if (keep[j]) nidx[j] = m++;
+  for (int j = 0; j < n; ++j) {
+    packed_parent[j] = -1;
+    index_map[j] = -1;
+  }
+  for (int j = 0; j < n; ++j)
+    if (keep[j]) {
+      packed_parent[nidx[j]] = parent[j] >= 0 ? nidx[parent[j]] : -1;
+      index_map[nidx[j]] = j;
+    }
+  if (scores)
+    for (int j = 0; j < n; ++j) scores[j] = q[j];
+  *count = m;
+  return SLA_OK;
+}
+
+int sla_tree_mask_to_parent(const uint64_t *mask, int32_t batch, int32_t n_nodes, int32_t *parent, int32_t *status,
+                            hipStream_t stream) {
+  if (!mask || !parent) return SLA_ERR_NULL;
+  if (batch < 1 || batch > (1 << 30) || n_nodes < 1 || n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+  sla::MaskArgs a{batch, n_nodes, mask, parent, status};
+  return hip_status(sla::launch_mask_to_parent(a, stream));
+}
+
+int sla_tree_mask_to_parent_host(const uint64_t *mask, int32_t n, int32_t *parent) {
+  if (!mask || !parent) return SLA_ERR_NULL;
+  if (n < 1 || n > SLA_MAX_NODES) return SLA_ERR_SHAPE;
+  std::vector<int32_t> p(n);
+  for (int i = 0; i < n; ++i) {
+    const uint64_t self = 1ull << i;
+    const uint64_t row = mask[i];
+    const uint64_t strict = row & ~self;
+    if (!(row & self) || (i < 63 && (row >> (i + 1)))) return SLA_ERR_TOPOLOGY;
+    p[i] = strict ? 63 - __builtin_clzll(strict) : -1;
+    if (row != ((p[i] >= 0 ? mask[p[i]] : 0ull) | self)) return SLA_ERR_TOPOLOGY;
+  }
+  for (int i = 0; i < n; ++i) parent[i] = p[i];
+  return SLA_OK;
 }
 
 int sla_topology(const int32_t *parent_idx, int32_t batch, int32_t n_nodes, int32_t *depth, uint64_t *anc,

@@ -69,6 +69,27 @@ struct ConvArgs {
   int32_t *status;
 };
 
+// Draft pruning and packing, one sequence per wavefront (n <= 64).
+struct PruneArgs {
+  int32_t B, n;
+  float tau;
+  int32_t budget;            // <= 0: no budget
+  const int32_t *parent;     // [B][n]
+  const float *logp;         // [B][n]
+  int32_t *packed_parent;    // [B][n]
+  int32_t *index_map;        // [B][n]
+  int32_t *count;            // [B]
+  float *scores;             // [B][n] or null
+  int32_t *status;           // [B] or null
+};
+
+struct MaskArgs {
+  int32_t B, n;
+  const uint64_t *mask;  // [B][n] rows
+  int32_t *parent;       // [B][n]
+  int32_t *status;       // [B] or null
+};
+
 struct TopologyArgs {
   int32_t B, n;
   const int32_t *parent;
@@ -87,5 +108,7 @@ hipError_t launch_verify_parallel(const VerifyArgs &a, int dtype, hipStream_t s)
 hipError_t launch_commit(const CommitArgs &a, int dtype, hipStream_t s);
 hipError_t launch_topology(const TopologyArgs &a, hipStream_t s);
 hipError_t launch_conv(const ConvArgs &a, int dtype, bool commit, hipStream_t s);
+hipError_t launch_prune(const PruneArgs &a, hipStream_t s);
+hipError_t launch_mask_to_parent(const MaskArgs &a, hipStream_t s);
 
 }  // namespace sla

@@ -22,7 +22,11 @@ proposal trees of the paper's evaluation, §8, which are not available):
     inputs x ~ N(0, 1) rounded to the activation dtype; committed conv state
     (earlier inputs) drawn the same way and held in fp32; depthwise weights
     [D][K] ~ U(-1/sqrt(K), 1/sqrt(K)) in fp32 (the default initialisation of a
-    depthwise conv1d), kernel size K = 4, no bias.
+    depthwise conv1d), kernel size K = 4, no bias;
+  * draft rollouts for pruning (§6.1): a per-level beam top-k rollout over a
+    random softmax per expanded node (32-token vocabulary, logits ~ N(0, 2^2));
+    each level expands the k best frontier nodes by path score, each with its
+    k most likely tokens, until the candidate count is reached.
 """
 from __future__ import annotations
 
@@ -257,3 +261,38 @@ def draw_conv_state(cfg: Config, layer: int, batch: int | None = None, channels:
     rng = _rng(base_seed(cfg), 5, layer)
     _, c32 = _to_dtype(rng.standard_normal((B, kernel - 1, D), dtype=np.float32), cfg.dtype)
     return np.ascontiguousarray(c32)
+
+
+# ---------------------------------------------------------------- draft rollouts
+def rollout(rng: np.random.Generator, n_cand: int, k: int = 4, vocab: int = 32, temp: float = 2.0):
+    """(parent [n_cand] int32, logp [n_cand] fp32) of one beam top-k rollout,
+    nodes in creation (topological) order."""
+    parent, logp, score = [], [], []
+
+    def children(of):
+        z = rng.standard_normal(vocab) * temp
+        lse = np.log(np.sum(np.exp(z - z.max()))) + z.max()
+        lp = np.sort(z - lse)[::-1][:k]
+        for x in lp:
+            if len(parent) < n_cand:
+                parent.append(of)
+                logp.append(float(x))
+                score.append(float(x) + (score[of] if of >= 0 else 0.0))
+
+    children(-1)
+    frontier = list(range(len(parent)))
+    while len(parent) < n_cand and frontier:
+        best = sorted(frontier, key=lambda v: -score[v])[:k]
+        start = len(parent)
+        for v in best:
+            children(v)
+        frontier = list(range(start, len(parent)))
+    return np.array(parent, np.int32), np.array(logp, np.float32)
+
+
+def draw_rollouts(cfg: Config, round_index: int = 0, batch: int | None = None, n_cand: int = 64, k: int = 4):
+    """Candidate sets of one round for every sequence: parent, logp [B][n_cand]."""
+    B = cfg.batch if batch is None else batch
+    rng = _rng(base_seed(cfg), round_index, 6)
+    rows = [rollout(rng, n_cand, k) for _ in range(B)]
+    return np.stack([r[0] for r in rows]), np.stack([r[1] for r in rows])
