@@ -9,6 +9,7 @@
 #include <vector>
 
 #include "kernels.hpp"
+#include "layer_ops.hpp"
 #include "sla.h"
 
 namespace {

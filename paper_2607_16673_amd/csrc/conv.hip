@@ -24,7 +24,7 @@
 // The bound is HBM: the draft rows and outputs stream once, the conv state
 // is read and written once, the weights are shared by every sequence.
 #include "device.hpp"
-#include "kernels.hpp"
+#include "layer_ops.hpp"
 
 namespace sla {
 namespace {

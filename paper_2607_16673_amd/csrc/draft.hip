@@ -16,7 +16,7 @@
 //   * packing: a kept node's new index is the number of kept nodes before it
 //     (ballot + popcount); its new parent is its parent's new index.
 #include "device.hpp"
-#include "kernels.hpp"
+#include "layer_ops.hpp"
 
 namespace sla {
 namespace {

@@ -42,7 +42,7 @@ COPY_TAG = "mul"  # the elementwise multiply of run_copy (not the fill before it
 # sources are stale
 SOURCES = {
     "gdn": ["verify_tile.hip", "verify_serial.hip", "commit.hip", "device.hpp", "kernels.hpp"],
-    "conv": ["conv.hip", "device.hpp", "kernels.hpp"],
+    "conv": ["conv.hip", "device.hpp", "layer_ops.hpp"],
 }
 
 
