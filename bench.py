@@ -104,9 +104,11 @@ def main():
                     help="launch eagerly from Python with HIP events around every launch")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters (if present)")
-    ap.add_argument("--study", default=None, choices=["tree-shapes"],
+    ap.add_argument("--study", default=None, choices=["tree-shapes", "fused-commit"],
                     help="tree-shapes: root-to-leaf replay, serial and parallel verification of synthetic "
-                         "top-k trees at the paper's target shape (8 heads, d_k = d_v = 256, batch 1)")
+                         "top-k trees at the paper's target shape (8 heads, d_k = d_v = 256, batch 1); "
+                         "fused-commit: fused commit-and-verify vs verify plus standalone commit for accepted "
+                         "lengths 1..8 at verify length 4 (the same shape)")
     ap.add_argument("--op", default="gdn", choices=["gdn", "conv", "prune"],
                     help="gdn: the recurrent-state verify+commit (the headline); conv: the layer's short "
                          "causal convolution with its conv-state commit, on the same drafts; prune: draft "
@@ -131,6 +133,8 @@ def main():
     B.lib()
     if args.study == "tree-shapes":
         return study_tree_shapes(args, torch, B, inputs, dev)
+    if args.study == "fused-commit":
+        return study_fused_commit(args, torch, B, inputs, dev)
     cfg = inputs.config(args.workload)
     if args.op == "conv":
         return run_conv(args, cfg, torch, B, inputs, dev)
@@ -518,12 +522,14 @@ def study_tree_shapes(args, torch, B, inputs, dev, trees_per_shape=8, reps=20):
     by root-to-leaf replay (one chain verification per root-to-leaf path,
     launched one after another from the committed state), by the serial route
     and by the parallel route; each timed as `reps` replays of a HIP graph
-    holding one tree's launches.  Also checks that the three agree."""
+    holding ten repetitions of one tree's launches (per-tree time = total /
+    (reps x 10), the gaps between kernels included).  Also checks that the
+    three agree."""
     H, dk, dv = 8, 256, 256
     rng = np.random.default_rng(4242)
     rows = []
 
-    def timed(launch):
+    def timed(launch, per_graph=10):
         launch()
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
@@ -531,7 +537,8 @@ def study_tree_shapes(args, torch, B, inputs, dev, trees_per_shape=8, reps=20):
         sc.wait_stream(torch.cuda.current_stream(dev))
         with torch.cuda.stream(sc):
             with torch.cuda.graph(g, stream=sc):
-                launch()
+                for _ in range(per_graph):
+                    launch()
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
@@ -542,7 +549,7 @@ def study_tree_shapes(args, torch, B, inputs, dev, trees_per_shape=8, reps=20):
             g.replay()
         e1.record(cur)
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) * 1e3 / reps  # us per tree
+        return e0.elapsed_time(e1) * 1e3 / (reps * per_graph)  # us per tree
 
     for k, depth, n in TREE_SHAPES:
         t = {"r2l": [], "serial": [], "parallel": []}
@@ -607,6 +614,93 @@ def study_tree_shapes(args, torch, B, inputs, dev, trees_per_shape=8, reps=20):
     print(json.dumps({"study": "tree-shapes", "shape": {"batch": 1, "heads": H, "d_k": dk, "d_v": dv,
                                                         "qkv_dtype": "bf16", "state_dtype": "f32"},
                       "trees_per_shape": trees_per_shape, "rows": rows}), flush=True)
+
+
+def study_fused_commit(args, torch, B, inputs, dev, reps=10, rounds=20):
+    """Delayed state update at the paper's target shape (batch 1, 8 heads,
+    d_k = d_v = 256, fp32 state, bf16 activations): per accepted length A in
+    1..8, the time of one round that commits the previous round's A accepted
+    nodes and verifies a 4-node chain, either fused (one sla_verify with the
+    path pending: one state read and write) or separate (sla_commit, then
+    sla_verify from the committed state).  Each route is a HIP graph of
+    `rounds` consecutive rounds, replayed `reps` times (per-round time =
+    total / (rounds x reps), the gaps between the kernels of a graph
+    included); the state keeps advancing."""
+    H, dk, dv, n_prev, n = 8, 256, 256, 8, 4
+    rng = np.random.default_rng(4343)
+
+    def bf(x):
+        return torch.from_numpy(np.ascontiguousarray(inputs.bf16_bits(x)).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    def unit(shape):
+        x = rng.standard_normal(shape)
+        return x / np.linalg.norm(x, axis=-1, keepdims=True)
+
+    def draft(m):
+        return dict(q=bf(unit((1, m, H, dk))), k=bf(unit((1, m, H, dk))), v=bf(rng.standard_normal((1, m, H, dv))),
+                    a=torch.from_numpy((1 / (1 + np.exp(-rng.uniform(2, 5, (1, m, H))))).astype(np.float32)).to(dev),
+                    b=torch.from_numpy((1 / (1 + np.exp(-rng.standard_normal((1, m, H))))).astype(np.float32)).to(dev),
+                    p=torch.arange(-1, m - 1, dtype=torch.int32, device=dev)[None])
+
+    prev, cur = draft(n_prev), draft(n)
+    S = torch.from_numpy((rng.standard_normal((1, H, dk, dv)) * 0.02).astype(np.float32)).to(dev)
+    fprev = B.Factors.empty(1, n_prev, H, dk, dv, torch.bfloat16, dev)
+    B.sla_verify(S, prev["q"], prev["k"], prev["v"], prev["a"], prev["b"], prev["p"],
+                 torch.empty(1, n_prev, H, dv, device=dev), fprev, topology="chain")
+    fcur = B.Factors.empty(1, n, H, dk, dv, torch.bfloat16, dev)
+    out = torch.empty(1, n, H, dv, device=dev)
+    # warm-up: clocks and caches settle before the first timed route
+    wpath = torch.arange(n_prev, dtype=torch.int32, device=dev)[None]
+    wlen = torch.tensor([4], dtype=torch.int32, device=dev)
+    for _ in range(200):
+        B.sla_verify(S, cur["q"], cur["k"], cur["v"], cur["a"], cur["b"], cur["p"], out, fcur,
+                     pending=(fprev, wpath, wlen), topology="chain")
+    torch.cuda.synchronize()
+    S.copy_(S / (1.0 + float(S.abs().max())))
+    rows = []
+    for A in range(1, 9):
+        path = torch.full((1, n_prev), -1, dtype=torch.int32, device=dev)
+        path[0, :A] = torch.arange(A, dtype=torch.int32, device=dev)
+        ln = torch.tensor([A], dtype=torch.int32, device=dev)
+        t = {}
+        for route in ["fused", "separate"]:
+            def launch():
+                if route == "fused":
+                    B.sla_verify(S, cur["q"], cur["k"], cur["v"], cur["a"], cur["b"], cur["p"], out, fcur,
+                                 pending=(fprev, path, ln), topology="chain")
+                else:
+                    B.sla_commit(S, fprev, path, ln)
+                    B.sla_verify(S, cur["q"], cur["k"], cur["v"], cur["a"], cur["b"], cur["p"], out, fcur,
+                                 topology="chain")
+            launch()
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            sc = torch.cuda.Stream(dev)
+            sc.wait_stream(torch.cuda.current_stream(dev))
+            with torch.cuda.stream(sc):
+                with torch.cuda.graph(g, stream=sc):
+                    for _ in range(rounds):
+                        launch()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            cs = torch.cuda.current_stream(dev)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(cs)
+            for _ in range(reps):
+                g.replay()
+            e1.record(cs)
+            torch.cuda.synchronize()
+            t[route] = e0.elapsed_time(e1) * 1e3 / (reps * rounds)
+            # keep the state in range: S drifts under repeated commits of the same records
+            S.copy_(S / (1.0 + float(S.abs().max())))
+        rows.append({"accepted": A, "fused_us": round(t["fused"], 2), "separate_us": round(t["separate"], 2),
+                     "separate_over_fused": round(t["separate"] / t["fused"], 2)})
+        log("accepted %d: fused %.2f us, separate %.2f us (%.2fx)" % (A, t["fused"], t["separate"],
+                                                                      t["separate"] / t["fused"]))
+    print(json.dumps({"study": "fused-commit", "shape": {"batch": 1, "heads": H, "d_k": dk, "d_v": dv,
+                                                         "verify_len": n, "qkv_dtype": "bf16", "state_dtype": "f32"},
+                      "rounds_per_graph": rounds, "reps": reps, "rows": rows}), flush=True)
 
 
 if __name__ == "__main__":
