@@ -83,7 +83,8 @@ extern "C" {
 
 typedef struct sla_shape {
   int32_t batch;     /* B >= 1                                              */
-  int32_t heads;     /* H >= 1                                              */
+  int32_t heads;     /* H >= 1, with 64 H max(d_k, d_v) 4 < 2^31 (one
+                        sequence's rows are addressed with 32-bit offsets) */
   int32_t d_k;       /* 64, 128 or 256                                      */
   int32_t d_v;       /* multiple of 16, 16..1024                            */
   int32_t n_nodes;   /* draft nodes per sequence, 1..SLA_MAX_NODES          */

@@ -42,6 +42,10 @@ int check_shape(const sla_shape *s) {
   if (!dk_ok(s->d_k)) return SLA_ERR_UNSUPPORTED;
   // grid sizes stay far inside 2^31 workgroups
   if ((uint64_t)s->batch * (uint64_t)s->heads * (uint64_t)(s->d_v / 16) > (1ull << 30)) return SLA_ERR_SHAPE;
+  // one sequence's rows of one tensor (all nodes and heads) are addressed with
+  // 32-bit byte offsets from the unit's first row
+  const uint64_t width = (uint64_t)(s->d_v > s->d_k ? s->d_v : s->d_k);
+  if ((uint64_t)SLA_MAX_NODES * (uint64_t)s->heads * width * 4 >= (1ull << 31)) return SLA_ERR_SHAPE;
   return SLA_OK;
 }
 

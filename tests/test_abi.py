@@ -142,6 +142,8 @@ def test_verify_argument_errors_return_before_launch():
     s.topology = 3
     assert _verify(s) == B.SLA_ERR_SHAPE
     assert _verify(B.make_shape(2, 4, 96, 128, 8)) == B.SLA_ERR_UNSUPPORTED
+    # a sequence's rows must stay addressable with 32-bit offsets
+    assert _verify(B.make_shape(1, 2048, 128, 4096, 8)) == B.SLA_ERR_SHAPE
     assert _verify(ok, route=9) == B.SLA_ERR_SHAPE
 
 
