@@ -186,6 +186,8 @@ __global__ __launch_bounds__(kConvWaves * kWave) void conv_verify_kernel(ConvArg
   // [K-1][2][64 x 16 B] (fp32, 8 channels per lane), then the verdict
   f32x4 *crows = reinterpret_cast<f32x4 *>(lds + (size_t)n * P * kWave * 16);
   int *s_err = reinterpret_cast<int *>(crows + KR * 2 * kWave);
+  // with several waves: [2K pieces][64 lanes], lane l's weights, 16 bytes per piece
+  f32x4 *wrows = reinterpret_cast<f32x4 *>(s_err + 4);
 
   // every wave: the parent row (lane j: node j), then its share of the draft
   // rows (j = w, w + nw, ...) straight into LDS
@@ -203,6 +205,13 @@ __global__ __launch_bounds__(kConvWaves * kWave) void conv_verify_kernel(ConvArg
     for (int q = 0; q < P; ++q)
       load_lds16(reinterpret_cast<const unsigned char *>(x + (size_t)j * a.D + c0) + 16 * q,
                  lds + (size_t)(j * P + q) * (kWave * 16));
+  // with several waves, the chunk's weights once per workgroup (a lane's 8 K
+  // floats are contiguous in [D][K]): piece v of every lane in one
+  // instruction, laid out [v][lane] so that the reads after the barrier are
+  // conflict-free.  A single wave reads its own straight into registers.
+  const bool wshared = nw > 1;
+  if (wshared)
+    for (int v = w; v < 2 * K; v += nw) load_lds16(a.weight + (size_t)c0 * K + 4 * v, wrows + v * kWave);
   int src[K];
   window_sources<K>(p, l, src);
 
@@ -245,31 +254,30 @@ __global__ __launch_bounds__(kConvWaves * kWave) void conv_verify_kernel(ConvArg
     if (l == 0) *s_err = err;
     if (a.status && l == 0 && blockIdx.x % nchunks == 0) a.status[b] = err;
   }
-  // weights and bias (shared by every sequence: L2 hits), after wave 0's
-  // commit so that its registers are free
-  float wt[K][kCpl], bias[kCpl];
+  float bias[kCpl];
+  if (a.bias) {
+    load_f8(a.bias + c0, bias);
+  } else {
+#pragma unroll
+    for (int e = 0; e < kCpl; ++e) bias[e] = 0.f;
+  }
+  __builtin_amdgcn_s_waitcnt(0);  // this wave's rows and weight pieces have landed
+  __syncthreads();                // and every other wave's, and the committed rows
+  if (*s_err != SLA_OK) return;
+  float wt[K][kCpl];
   {
     float flat[K * kCpl];
     const f32x4 *wv = reinterpret_cast<const f32x4 *>(a.weight + (size_t)c0 * K);
 #pragma unroll
-    for (int v = 0; v < K * kCpl / 4; ++v) {
-      const f32x4 t = wv[v];
+    for (int v = 0; v < 2 * K; ++v) {
+      const f32x4 t = wshared ? wrows[v * kWave + l] : wv[v];
       flat[4 * v] = t.x; flat[4 * v + 1] = t.y; flat[4 * v + 2] = t.z; flat[4 * v + 3] = t.w;
     }
 #pragma unroll
     for (int e = 0; e < kCpl; ++e)
 #pragma unroll
       for (int i = 0; i < K; ++i) wt[i][e] = flat[e * K + i];
-    if (a.bias) {
-      load_f8(a.bias + c0, bias);
-    } else {
-#pragma unroll
-      for (int e = 0; e < kCpl; ++e) bias[e] = 0.f;
-    }
   }
-  __builtin_amdgcn_s_waitcnt(0);  // this wave's rows have landed
-  __syncthreads();                // and every other wave's, and the committed rows
-  if (*s_err != SLA_OK) return;
 
   XT *y = static_cast<XT *>(a.y) + (size_t)b * n * a.D + c0;
   const u32x4 *rows = reinterpret_cast<const u32x4 *>(lds) + l;
@@ -343,15 +351,17 @@ hipError_t launch_k(const ConvArgs &a, bool commit, hipStream_t s) {
     return hipGetLastError();
   }
   const int K1 = K > 1 ? K - 1 : 1;
-  const size_t lds = (size_t)a.n * kPieces<XT> * kWave * 16 + (size_t)K1 * 2 * kWave * 16 + 16;
+  // up to four waves split the draft's nodes (a 1-node draft takes one); with
+  // several, the chunk's weights are staged in LDS once
+  const int waves = a.n < kConvWaves ? a.n : kConvWaves;
+  const size_t lds = (size_t)a.n * kPieces<XT> * kWave * 16 + (size_t)K1 * 2 * kWave * 16 + 16 +
+                     (waves > 1 ? (size_t)2 * K * kWave * 16 : 0);
   auto kern = conv_verify_kernel<XT, K>;
   if (lds > 64 * 1024) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  // up to four waves split the draft's nodes (a 1-node draft takes one)
-  const int waves = a.n < kConvWaves ? a.n : kConvWaves;
   hipLaunchKernelGGL(kern, grid, dim3(waves * kWave), lds, s, a);
   return hipGetLastError();
 }
