@@ -23,6 +23,7 @@ struct VerifyArgs {
   bool chain;
   bool has_pending;
   bool late_state;  // parallel route: issue the state reads after the first barrier
+  bool stagger;     // parallel route: hold the state reads back briefly (a full round of workgroups)
   float *state;
   PendingArgs pend;
   const void *q, *k, *v;

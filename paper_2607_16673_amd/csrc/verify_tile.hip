@@ -203,6 +203,11 @@ void verify_tile_kernel(VerifyArgs a) {
   float hfa[KS][8], hfb[KS][8];  // hfb: the next tile's state (prefetching form only)
   uint32_t vraw[NT][4];  // bf16 bit patterns, widened where they are used
   if (live(t0)) {
+    // a full round of workgroups: hold the state reads back about a
+    // microsecond (40 x 64 cycles), so that every workgroup's setup reads
+    // and [Q; K] enter the memory queue ahead of the state (measured -1%
+    // per launch; 80 and 127 were slower)
+    if (a.stagger) __builtin_amdgcn_s_sleep(40);
     if (!a.late_state) load_state(t0, hfa);
     load_values(t0, vraw);
   }
@@ -676,7 +681,9 @@ hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
   const int ntiles = (a.dv + L::kTileCols - 1) / L::kTileCols;
   const size_t groups = (size_t)a.B * a.H * ((ntiles + TPW - 1) / TPW);
   VerifyArgs b = a;
-  b.late_state = groups >= (size_t)kLateRounds * kSlotsPerCu * device_cus();
+  const size_t slots = (size_t)kSlotsPerCu * device_cus();
+  b.late_state = groups >= (size_t)kLateRounds * slots;
+  b.stagger = !b.late_state && groups >= slots;
   hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3((CW + 1) * kWave), lds, s, b);
   return hipGetLastError();
 }
