@@ -138,6 +138,57 @@ def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, jso
     return {key: entry}
 
 
+MFMA_COUNTERS = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_BUSY_CU_CYCLES", "GRBM_GUI_ACTIVE"]
+
+
+def summarize_mfma(out_dir: str, workload: str, skip: int, json_path: str, kernel: str = KERNEL_TAG,
+                   simds: int = 1024) -> dict:
+    """Matrix-core use of the verify kernel from one rocprofv3 --pmc pass with
+    MFMA_COUNTERS, per launch: MFMA busy cycles per SIMD (busy cycles summed
+    over the SIMDs / simds) and the bf16 MFMA operations
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 counts multiply and add operations / 512).
+    GRBM_GUI_ACTIVE is kept for reference only: under counter collection it
+    spans more than the kernel (dispatches are serialised and sampled), so
+    utilisation is taken against the kernel-trace duration instead."""
+    files = glob.glob(os.path.join(out_dir, "**", "*counter_collection.csv"), recursive=True)
+    if len(files) != 1:
+        raise RuntimeError("expected one counter file under %s, found %d" % (out_dir, len(files)))
+    acc = {}
+    order = []
+    with open(files[0], newline="") as f:
+        for r in csv.DictReader(f):
+            if kernel.lower() not in r.get("Kernel_Name", "").lower():
+                continue
+            d = r.get("Dispatch_Id") or r.get("Correlation_Id")
+            if d not in acc:
+                acc[d] = {}
+                order.append(d)
+            c = r["Counter_Name"]
+            v = float(r["Counter_Value"])
+            # GRBM_GUI_ACTIVE is per XCD: the launch's span is the largest one
+            acc[d][c] = max(acc[d].get(c, 0.0), v) if c == "GRBM_GUI_ACTIVE" else acc[d].get(c, 0.0) + v
+    rows = [acc[d] for d in order][skip:]
+    if not rows:
+        raise ValueError("no dispatch of %r" % kernel)
+    mean = {c: sum(r.get(c, 0.0) for r in rows) / len(rows) for c in MFMA_COUNTERS}
+    entry = {
+        "kernel": kernel, "dispatches": len(rows), "simds": simds,
+        "mfma_busy_cycles_per_simd": mean["SQ_VALU_MFMA_BUSY_CYCLES"] / simds,
+        "bf16_mfma_flops": mean["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512,
+        "gui_active_cycles_under_collection": mean["GRBM_GUI_ACTIVE"],
+        "source_sha256": source_digest("gdn"),
+    }
+    data = {}
+    if os.path.exists(json_path):
+        with open(json_path) as f:
+            data = json.load(f)
+    data["%s/mfma" % workload] = entry
+    with open(json_path, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+        f.write("\n")
+    return entry
+
+
 def main(argv=None) -> None:
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -152,9 +203,16 @@ def main(argv=None) -> None:
     s.add_argument("--skip", type=int, default=0,
                    help="leading verify dispatches to ignore (the first step has no pending path)")
     s.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    m = sub.add_parser("mfma")
+    m.add_argument("--out-dir", required=True)
+    m.add_argument("--workload", required=True)
+    m.add_argument("--skip", type=int, default=0)
+    m.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     a = ap.parse_args(argv)
     if a.cmd == "copy":
         run_copy(a.mib)
+    elif a.cmd == "mfma":
+        print(json.dumps(summarize_mfma(a.out_dir, a.workload, a.skip, a.json), indent=1))
     else:
         print(json.dumps(summarize(a.out_dir, a.workload, a.route, a.mode, a.skip, a.json, a.kernel), indent=1))
 
