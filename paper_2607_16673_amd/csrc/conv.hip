@@ -73,9 +73,12 @@ __device__ __forceinline__ void store_row(bf16 *y, const float (&f)[kCpl]) {
   __builtin_nontemporal_store(o, reinterpret_cast<u32x4 *>(y));
 }
 
+// fp32 rows: a lane's 32 bytes go out as two 16-byte stores, so each store
+// instruction covers half of every line; the default policy lets the L2 merge
+// the halves (a streaming hint writes them separately)
 __device__ __forceinline__ void store_row(float *y, const float (&f)[kCpl]) {
-  __builtin_nontemporal_store(f32x4{f[0], f[1], f[2], f[3]}, reinterpret_cast<f32x4 *>(y));
-  __builtin_nontemporal_store(f32x4{f[4], f[5], f[6], f[7]}, reinterpret_cast<f32x4 *>(y) + 1);
+  reinterpret_cast<f32x4 *>(y)[0] = f32x4{f[0], f[1], f[2], f[3]};
+  reinterpret_cast<f32x4 *>(y)[1] = f32x4{f[4], f[5], f[6], f[7]};
 }
 
 template <typename XT>
