@@ -204,11 +204,12 @@ void verify_tile_kernel(VerifyArgs a) {
   float hfa[KS][8], hfb[KS][8];  // hfb: the next tile's state (prefetching form only)
   uint32_t vraw[NT][4];  // bf16 bit patterns, widened where they are used
   if (live(t0)) {
-    // a full round of workgroups: hold the state reads back about a
-    // microsecond (40 x 64 cycles), so that every workgroup's setup reads
-    // and [Q; K] enter the memory queue ahead of the state (measured -1%
-    // per launch; 80 and 127 were slower)
-    if (a.stagger) __builtin_amdgcn_s_sleep(40);
+    // a full round of workgroups: hold the state reads back about two
+    // microseconds (80 x 64 cycles), so that every workgroup's setup reads
+    // and [Q; K] enter the memory queue ahead of the state (measured per
+    // launch against no delay: 20 -> +1.6%, 40 -> -1.0%, 64 -> -1.7%,
+    // 80 -> -2.1%, 100 -> -1.7%)
+    if (a.stagger) __builtin_amdgcn_s_sleep(80);
     if (!a.late_state) load_state(t0, hfa);
     load_values(t0, vraw);
   }
