@@ -667,11 +667,12 @@ int device_cus() {
 
 // The state reads of a workgroup normally go out first, so that they overlap
 // the setup wave's dependent reads.  When the launch holds at least
-// kLateRounds rounds of workgroups (counting kSlotsPerCu resident per CU),
-// they go out after the first barrier instead: measured 4.5% faster on the
-// 1-node decode chain at batch 256, 1% slower at one round.
+// kLateRounds rounds of workgroups (resident workgroups per CU from the
+// occupancy of the kernel instantiation), they go out after the first
+// barrier instead: measured 4.5% faster on the 1-node decode chain at batch
+// 256, 1% slower at one round.  At one to kLateRounds rounds the column waves
+// hold them back briefly instead (stagger).
 constexpr int kLateRounds = 4;
-constexpr int kSlotsPerCu = 4;
 
 template <int DK, int NP, int CW, int TPW>
 hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
@@ -687,7 +688,13 @@ hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
   const int ntiles = (a.dv + L::kTileCols - 1) / L::kTileCols;
   const size_t groups = (size_t)a.B * a.H * ((ntiles + TPW - 1) / TPW);
   VerifyArgs b = a;
-  const size_t slots = (size_t)kSlotsPerCu * device_cus();
+  // resident workgroups per CU for this instantiation (registers, LDS, waves)
+  static const int per_cu = [&] {
+    int k = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&k, kern, (CW + 1) * kWave, lds) != hipSuccess || k < 1) k = 1;
+    return k;
+  }();
+  const size_t slots = (size_t)per_cu * device_cus();
   b.late_state = groups >= (size_t)kLateRounds * slots;
   b.stagger = !b.late_state && groups >= slots;
   hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3((CW + 1) * kWave), lds, s, b);
