@@ -25,6 +25,13 @@ ERR_SHAPE = -2
 ERR_TOPOLOGY = -4
 ERR_PATH = -5
 
+# Layer families (the factor-record remark closing §5.1); see oracle.c.
+GDN = 0
+DELTANET = 1
+DECAY = 2
+GLA = 3
+FAMILIES = {"gdn": GDN, "deltanet": DELTANET, "decay": DECAY, "gla": GLA}
+
 _dp = ctypes.POINTER(ctypes.c_double)
 _ip = ctypes.POINTER(ctypes.c_int32)
 _up = ctypes.POINTER(ctypes.c_uint64)
@@ -54,6 +61,11 @@ def _load():
     lib.oracle_verify.restype = ctypes.c_int
     lib.oracle_commit.argtypes = [ctypes.c_int] * 5 + [_dp] * 5 + [_ip, _ip, ctypes.c_int, _ip, _ip]
     lib.oracle_commit.restype = ctypes.c_int
+    lib.oracle_layer_step.argtypes = [ctypes.c_int] * 3 + [_dp] * 4 + [ctypes.c_double, _dp]
+    lib.oracle_verify_family.argtypes = [ctypes.c_int] * 6 + [_dp] * 6 + [_ip, _dp, _ip]
+    lib.oracle_verify_family.restype = ctypes.c_int
+    lib.oracle_commit_family.argtypes = [ctypes.c_int] * 6 + [_dp] * 5 + [_ip, _ip, ctypes.c_int, _ip, _ip]
+    lib.oracle_commit_family.restype = ctypes.c_int
     lib.oracle_conv_verify.argtypes = [ctypes.c_int] * 4 + [_dp] * 4 + [ctypes.c_int, _ip, _dp, _ip]
     lib.oracle_conv_verify.restype = ctypes.c_int
     lib.oracle_conv_commit.argtypes = [ctypes.c_int] * 4 + [_dp, _dp, _ip, _ip, ctypes.c_int, _ip, _ip]
@@ -92,6 +104,28 @@ def gdn_step(Hs, k, v, alpha, beta):
     scratch = np.zeros(dv)
     lib.oracle_gdn_step(dk, dv, _p(H, _dp), _p(k, _dp), _p(v, _dp), float(alpha),
                         float(beta), _p(scratch, _dp))
+    return H
+
+
+def _family(f):
+    return FAMILIES[f] if isinstance(f, str) else int(f)
+
+
+def layer_step(Hs, k, v, gate, beta, family=GDN):
+    """One step of a layer family on H = S^T ([dk][dv]); returns a copy.
+
+    gate: alpha (GDN, DECAY), the dk per-key gates (GLA), unused (DELTANET);
+    beta: unused for DECAY and GLA."""
+    lib = _load()
+    fam = _family(family)
+    H = _f64(Hs).copy()
+    dk, dv = H.shape
+    k = _f64(k)
+    v = _f64(v)
+    g = _f64(np.reshape(gate if gate is not None else 0.0, (-1,)))
+    scratch = np.zeros(dv)
+    lib.oracle_layer_step(fam, dk, dv, _p(H, _dp), _p(k, _dp), _p(v, _dp), _p(g, _dp),
+                          float(beta if beta is not None else 0.0), _p(scratch, _dp))
     return H
 
 
@@ -146,46 +180,70 @@ def validate_path(parent, path, length) -> int:
     return _load().oracle_validate_path(_p(p, _ip), len(p), _p(pa, _ip), int(length))
 
 
-def verify(state, q, k, v, alpha, beta, parent):
+def _gates(family, alpha, beta, B, n, H, dk):
+    """fp64 gate and beta arrays (None where the family does not read them)."""
+    if family == DELTANET:
+        g = None
+    else:
+        g = _f64(alpha)
+        want = (B, n, H, dk) if family == GLA else (B, n, H)
+        assert g.shape == want, (g.shape, want)
+    if family in (DECAY, GLA):
+        bt = None
+    else:
+        bt = _f64(beta)
+        assert bt.shape == (B, n, H)
+    return g, bt
+
+
+def _opt(a):
+    return _p(a, _dp) if a is not None else None
+
+
+def verify(state, q, k, v, alpha, beta, parent, family=GDN):
     """Per-node outputs by definition (§4; tree mask §4.2).
 
-    state [B][H][dk][dv]; q,k [B][n][H][dk]; v [B][n][H][dv]; alpha,beta
-    [B][n][H]; parent [B][n].  Returns (out [B][n][H][dv] fp64, status [B])."""
+    state [B][H][dk][dv]; q,k [B][n][H][dk]; v [B][n][H][dv]; parent [B][n].
+    alpha: [B][n][H] (GDN, DECAY), [B][n][H][dk] per-key gates (GLA), or None
+    (DELTANET); beta: [B][n][H] (GDN, DELTANET) or None (DECAY, GLA).
+    Returns (out [B][n][H][dv] fp64, status [B])."""
     lib = _load()
+    fam = _family(family)
     S = _f64(state)
     B, H, dk, dv = S.shape
     q, k, v = _f64(q), _f64(k), _f64(v)
     n = q.shape[1]
-    a, bt = _f64(alpha), _f64(beta)
+    g, bt = _gates(fam, alpha, beta, B, n, H, dk)
     par = _i32(parent).reshape(B, n)
     assert q.shape == (B, n, H, dk) and k.shape == (B, n, H, dk) and v.shape == (B, n, H, dv)
-    assert a.shape == (B, n, H) and bt.shape == (B, n, H)
     out = np.zeros((B, n, H, dv))
     status = np.zeros(B, np.int32)
-    lib.oracle_verify(B, H, dk, dv, n, _p(S, _dp), _p(q, _dp), _p(k, _dp), _p(v, _dp),
-                      _p(a, _dp), _p(bt, _dp), _p(par, _ip), _p(out, _dp), _p(status, _ip))
+    lib.oracle_verify_family(fam, B, H, dk, dv, n, _p(S, _dp), _p(q, _dp), _p(k, _dp), _p(v, _dp),
+                             _opt(g), _opt(bt), _p(par, _ip), _p(out, _dp), _p(status, _ip))
     return out, status
 
 
-def commit(state, k, v, alpha, beta, parent, path, length):
+def commit(state, k, v, alpha, beta, parent, path, length, family=GDN):
     """Committed state after decoding the accepted tokens one by one (§5.1-5.2).
 
-    path [B][stride] (-1 padded), length [B].  Returns (state', status)."""
+    path [B][stride] (-1 padded), length [B]; alpha and beta as for verify.
+    Returns (state', status)."""
     lib = _load()
+    fam = _family(family)
     S = _f64(state).copy()
     B, H, dk, dv = S.shape
     k, v = _f64(k), _f64(v)
     n = k.shape[1]
-    a, bt = _f64(alpha), _f64(beta)
+    g, bt = _gates(fam, alpha, beta, B, n, H, dk)
     par = _i32(parent).reshape(B, n)
     pa = _i32(path).reshape(B, -1)
     if pa.shape[1] == 0:
         pa = np.full((B, 1), -1, np.int32)
     ln = _i32(length).reshape(B)
     status = np.zeros(B, np.int32)
-    lib.oracle_commit(B, H, dk, dv, n, _p(S, _dp), _p(k, _dp), _p(v, _dp), _p(a, _dp),
-                      _p(bt, _dp), _p(par, _ip), _p(pa, _ip), pa.shape[1], _p(ln, _ip),
-                      _p(status, _ip))
+    lib.oracle_commit_family(fam, B, H, dk, dv, n, _p(S, _dp), _p(k, _dp), _p(v, _dp), _opt(g),
+                             _opt(bt), _p(par, _ip), _p(pa, _ip), pa.shape[1], _p(ln, _ip),
+                             _p(status, _ip))
     return S, status
 
 

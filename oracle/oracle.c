@@ -27,6 +27,9 @@
  *   - Commit (§5.1 "state recovery", §5.2): the durable state after
  *     accepting the path a_1..a_A is the state after decoding those tokens
  *     one at a time, starting from the committed state.
+ *   - The same definitions for the other stateful layer families whose
+ *     factor records §5.1 lists (DeltaNet, scalar decay without the delta
+ *     rule, GLA's per-key gates); see the section on layer families.
  *   - The short causal convolution in front of the recurrent core and its
  *     conv state (see the section at the end of this file).
  *   - Topology (§4.2 tree mask, §7 parent array): depth, inclusive
@@ -164,15 +167,71 @@ int oracle_validate_path(const int32_t *parent, int n, const int32_t *path, int 
   return OR_OK;
 }
 
+/* ------------------------------------------------------------------------
+ * Layer families.  §5.1 closes with the remark that stateful linear layers
+ * keep different factor records: GLA-style layers a key, a value and a
+ * gate but no delta-rule beta; DeltaNet a key, a value and beta but no
+ * decay; Mamba-style selective SSMs their own decay parameters in place of
+ * the delta rule.  The steps those layers take, on H = S^T ([dk][dv]):
+ *   OR_FAM_GDN       H' = alpha (H - beta k (k^T H)) + beta k v^T
+ *   OR_FAM_DELTANET  H' = H - beta k (k^T H) + beta k v^T     (no decay)
+ *   OR_FAM_DECAY     H' = alpha H + k v^T                      (scalar decay,
+ *                                                               no delta rule)
+ *   OR_FAM_GLA       H'[i][c] = g[i] H[i][c] + k[i] v[c]       (one gate per
+ *                                                               key dimension)
+ * In the S orientation the GLA gate multiplies S from the right,
+ * S' = S diag(g) + v k^T.  `gate` points at alpha (GDN, DECAY) or at the dk
+ * gates (GLA) and is unused for DELTANET; beta is unused for DECAY and GLA.
+ * Verification and commit are the same definitions for every family: node
+ * j's output is read from the state after the steps of P(j), and a commit
+ * decodes the accepted tokens one at a time. */
+#define OR_FAM_GDN 0
+#define OR_FAM_DELTANET 1
+#define OR_FAM_DECAY 2
+#define OR_FAM_GLA 3
+
+static int family_ok(int family) { return family >= OR_FAM_GDN && family <= OR_FAM_GLA; }
+
+/* Gates per (b, j, h) record: dk for GLA, 1 otherwise. */
+static size_t gate_width(int family, int dk) { return family == OR_FAM_GLA ? (size_t)dk : 1; }
+
+void oracle_layer_step(int family, int dk, int dv, double *H, const double *k, const double *v,
+                       const double *gate, double beta, double *kH) {
+  switch (family) {
+    case OR_FAM_GDN:
+      oracle_gdn_step(dk, dv, H, k, v, gate[0], beta, kH);
+      return;
+    case OR_FAM_DELTANET:
+      for (int c = 0; c < dv; ++c) {
+        double s = 0.0;
+        for (int i = 0; i < dk; ++i) s += k[i] * H[(size_t)i * dv + c];
+        kH[c] = s;
+      }
+      for (int i = 0; i < dk; ++i)
+        for (int c = 0; c < dv; ++c) H[(size_t)i * dv + c] += beta * k[i] * (v[c] - kH[c]);
+      return;
+    case OR_FAM_DECAY:
+      for (int i = 0; i < dk; ++i)
+        for (int c = 0; c < dv; ++c) H[(size_t)i * dv + c] = gate[0] * H[(size_t)i * dv + c] + k[i] * v[c];
+      return;
+    case OR_FAM_GLA:
+      for (int i = 0; i < dk; ++i)
+        for (int c = 0; c < dv; ++c) H[(size_t)i * dv + c] = gate[i] * H[(size_t)i * dv + c] + k[i] * v[c];
+      return;
+  }
+}
+
 /* Verification by definition.  For every (b, h) and node j: copy the
- * committed state, apply the GDN steps of the nodes of P(j) root first,
- * then read out o_j = H^T q_j.  status[b] (nullable) gets the per-sequence
- * topology verdict; invalid sequences produce no output. */
-int oracle_verify(int B, int H, int dk, int dv, int n, const double *state,
-                  const double *q, const double *k, const double *v,
-                  const double *alpha, const double *beta, const int32_t *parent,
-                  double *out, int32_t *status) {
-  if (B < 1 || H < 1 || dk < 1 || dv < 1 || n < 1 || n > OR_MAX_NODES) return OR_ERR_SHAPE;
+ * committed state, apply the steps of the nodes of P(j) root first, then
+ * read out o_j = H^T q_j.  status[b] (nullable) gets the per-sequence
+ * topology verdict; invalid sequences produce no output.  gate is
+ * [B][n][H] (or [B][n][H][dk] for GLA), NULL for DELTANET; beta [B][n][H],
+ * NULL for DECAY and GLA. */
+int oracle_verify_family(int family, int B, int H, int dk, int dv, int n, const double *state,
+                         const double *q, const double *k, const double *v, const double *gate,
+                         const double *beta, const int32_t *parent, double *out, int32_t *status) {
+  if (B < 1 || H < 1 || dk < 1 || dv < 1 || n < 1 || n > OR_MAX_NODES || !family_ok(family)) return OR_ERR_SHAPE;
+  const size_t gw = gate_width(family, dk);
   int bad = 0;
   for (int b = 0; b < B; ++b) {
     int st = oracle_check_parent(parent + (size_t)b * n, n);
@@ -193,7 +252,8 @@ int oracle_verify(int B, int H, int dk, int dv, int n, const double *state,
         memcpy(Hw, H0, sizeof(double) * (size_t)dk * dv);
         for (int t = 0; t < len; ++t) {
           size_t a = ((size_t)b * n + path[t]) * H + h;
-          oracle_gdn_step(dk, dv, Hw, k + a * dk, v + a * dv, alpha[a], beta[a], kH);
+          oracle_layer_step(family, dk, dv, Hw, k + a * dk, v + a * dv, gate ? gate + a * gw : NULL,
+                            beta ? beta[a] : 0.0, kH);
         }
         size_t jj = ((size_t)b * n + j) * H + h;
         oracle_readout(dk, dv, Hw, q + jj * dk, out + jj * dv);
@@ -203,15 +263,25 @@ int oracle_verify(int B, int H, int dk, int dv, int n, const double *state,
   return bad ? OR_ERR_TOPOLOGY : OR_OK;
 }
 
+/* The GDN case with the original argument order. */
+int oracle_verify(int B, int H, int dk, int dv, int n, const double *state,
+                  const double *q, const double *k, const double *v,
+                  const double *alpha, const double *beta, const int32_t *parent,
+                  double *out, int32_t *status) {
+  return oracle_verify_family(OR_FAM_GDN, B, H, dk, dv, n, state, q, k, v, alpha, beta, parent, out, status);
+}
+
 /* Commit by definition: for every (b, h), starting from the committed
  * state, decode the accepted tokens path[b][0..len[b]) one at a time with
- * the GDN step, in place.  Sequences whose path is not a root path of their
- * draft are left untouched and get OR_ERR_PATH in status[b] (nullable). */
-int oracle_commit(int B, int H, int dk, int dv, int n, double *state,
-                  const double *k, const double *v, const double *alpha,
-                  const double *beta, const int32_t *parent, const int32_t *path,
-                  int path_stride, const int32_t *len, int32_t *status) {
-  if (B < 1 || H < 1 || dk < 1 || dv < 1 || n < 1 || n > OR_MAX_NODES) return OR_ERR_SHAPE;
+ * the family's step, in place.  Sequences whose path is not a root path of
+ * their draft are left untouched and get OR_ERR_PATH in status[b]
+ * (nullable).  gate and beta as for verification. */
+int oracle_commit_family(int family, int B, int H, int dk, int dv, int n, double *state,
+                         const double *k, const double *v, const double *gate,
+                         const double *beta, const int32_t *parent, const int32_t *path,
+                         int path_stride, const int32_t *len, int32_t *status) {
+  if (B < 1 || H < 1 || dk < 1 || dv < 1 || n < 1 || n > OR_MAX_NODES || !family_ok(family)) return OR_ERR_SHAPE;
+  const size_t gw = gate_width(family, dk);
   int bad = 0;
   for (int b = 0; b < B; ++b) {
     int st = oracle_check_parent(parent + (size_t)b * n, n);
@@ -231,11 +301,20 @@ int oracle_commit(int B, int H, int dk, int dv, int n, double *state,
       double *Hs = state + ((size_t)b * H + h) * dk * dv;
       for (int t = 0; t < len[b]; ++t) {
         size_t a = ((size_t)b * n + pth[t]) * H + h;
-        oracle_gdn_step(dk, dv, Hs, k + a * dk, v + a * dv, alpha[a], beta[a], kH);
+        oracle_layer_step(family, dk, dv, Hs, k + a * dk, v + a * dv, gate ? gate + a * gw : NULL,
+                          beta ? beta[a] : 0.0, kH);
       }
       free(kH);
     }
   return bad ? OR_ERR_PATH : OR_OK;
+}
+
+int oracle_commit(int B, int H, int dk, int dv, int n, double *state,
+                  const double *k, const double *v, const double *alpha,
+                  const double *beta, const int32_t *parent, const int32_t *path,
+                  int path_stride, const int32_t *len, int32_t *status) {
+  return oracle_commit_family(OR_FAM_GDN, B, H, dk, dv, n, state, k, v, alpha, beta, parent, path,
+                              path_stride, len, status);
 }
 
 /* ------------------------------------------------------------------------
