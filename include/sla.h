@@ -81,6 +81,25 @@ extern "C" {
 
 #define SLA_MAX_NODES 64
 
+/* Layer family of the recurrent core.  Stateful linear layers keep the
+ * factors their own state advance consumes (the remark closing §5.1): GDN
+ * a key, a value, a decay and beta; DeltaNet a key, a value and beta but no
+ * decay; GLA-style layers a key, a value and a gate but no beta; selective
+ * SSMs a decay in place of the delta rule.  With g the gate:
+ *   GDN       S <- alpha S (I - beta k k^T) + beta v k^T   (gated delta rule)
+ *   DELTANET  S <- S (I - beta k k^T) + beta v k^T         (no decay)
+ *   DECAY     S <- alpha S + v k^T                          (scalar decay, no
+ *                                                            delta rule: the
+ *                                                            selective-SSM form)
+ *   GLA       S <- S diag(g) + v k^T                        (one gate per key
+ *                                                            dimension)
+ * Verification, factor records and commit follow the same definitions for
+ * every family (o_j = S_j q_j after the steps of P(j)). */
+#define SLA_FAMILY_GDN 0
+#define SLA_FAMILY_DELTANET 1
+#define SLA_FAMILY_DECAY 2
+#define SLA_FAMILY_GLA 3
+
 typedef struct sla_shape {
   int32_t batch;     /* B >= 1                                              */
   int32_t heads;     /* H >= 1, with 64 H max(d_k, d_v) 4 < 2^31 (one
@@ -90,17 +109,23 @@ typedef struct sla_shape {
   int32_t n_nodes;   /* draft nodes per sequence, 1..SLA_MAX_NODES          */
   int32_t qkv_dtype; /* SLA_DTYPE_F32 or SLA_DTYPE_BF16                     */
   int32_t topology;  /* SLA_TOPO_TREE or SLA_TOPO_CHAIN                     */
+  int32_t family;    /* SLA_FAMILY_*; 0 (GDN) when zero-initialised         */
 } sla_shape;
 
 /* Factor store (§5.1, factor buffering).  One record per node and head:
  *   k     [B][n][H][d_k]  the node's key, in the activation dtype;
- *   u     [B][n][H][d_v]  fp32 corrected value u_j = beta_j (v_j - alpha_j
- *                         S_par k_j), with S_par the state of node j's parent;
- *   alpha [B][n][H]       fp32 decay alpha_j;
+ *   u     [B][n][H][d_v]  fp32 value the state advance writes: the corrected
+ *                         value u_j = beta_j (v_j - alpha_j S_par k_j) of the
+ *                         delta-rule families (alpha = 1 for DELTANET), with
+ *                         S_par the state of node j's parent; v_j itself for
+ *                         DECAY and GLA;
+ *   alpha [B][n][H]       fp32 gate: alpha_j (GDN, DECAY), 1 (DELTANET);
+ *         [B][n][H][d_k]  for GLA, the per-key gates g_j;
  *   parent[B][n]          int32 copy of the draft's parent array.
- * With these, node j's state is S_j = alpha_j S_par + u_j k_j^T, so an
- * accepted path is committed by rank-one updates alone (no reductions).
- * All four are device memory written by sla_verify. */
+ * With these, node j's state is S_j = S_par diag(g_j) + u_j k_j^T (a scalar
+ * gate: alpha_j S_par + u_j k_j^T), so an accepted path is committed by
+ * rank-one updates alone (no reductions).  All four are device memory
+ * written by sla_verify; sla_factors_bytes gives their total size. */
 typedef struct sla_factors {
   void *k;
   float *u;
@@ -138,12 +163,18 @@ typedef struct sla_pending {
  *           factor stores), else SLA_ERR_ALIAS.
  *   q, k    device [B][n][H][d_k], shape->qkv_dtype.
  *   v       device [B][n][H][d_v], shape->qkv_dtype.
- *   alpha, beta  device fp32 [B][n][H]; decay and delta-rule strength.
+ *   alpha   device fp32 [B][n][H], the decay (GDN, DECAY); [B][n][H][d_k],
+ *           the per-key gates (GLA); not read for DELTANET (may be NULL).
+ *   beta    device fp32 [B][n][H], the delta-rule strength (GDN, DELTANET);
+ *           not read for DECAY and GLA (may be NULL).
  *   parent_idx   device int32 [B][n]; topological order required.
  *   out     device fp32 [B][n][H][d_v]; o_j = S_j q_j.
  *   factors device factor store written for this draft (see sla_factors).
  *   status  device int32 [B] or NULL: 0, SLA_ERR_TOPOLOGY or SLA_ERR_PATH.
- *   route   SLA_ROUTE_*.
+ *   route   SLA_ROUTE_*.  GLA runs on the serial route only (PARALLEL:
+ *           SLA_ERR_UNSUPPORTED; AUTO takes SERIAL), and the serial route
+ *           stages k, q and the gates of all nodes on chip: for GLA at
+ *           d_k = 256 that limits n to 50 (SLA_ERR_UNSUPPORTED above).
  * Returns SLA_OK once the work is enqueued, or a negative error code. */
 int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pending *pending,
                const void *q, const void *k, const void *v, const float *alpha,
@@ -151,8 +182,9 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
                const sla_factors *factors, int32_t *status, hipStream_t stream);
 
 /* sla_commit -- immediate state update (§5.2): apply the accepted path's
- * factor records to the state in place, S <- alpha_a S + u_a k_a^T for each
- * accepted node a, root first.  shape->n_nodes is the n of the factors; path
+ * factor records to the state in place, S <- S diag(g_a) + u_a k_a^T for
+ * each accepted node a, root first (a scalar gate: alpha_a S + u_a k_a^T);
+ * shape->family says which gate layout the factors hold.  shape->n_nodes is the n of the factors; path
  * and len are as in sla_pending.  len[b] = 0 leaves sequence b untouched.
  * The per-element arithmetic is the same as the pending prologue of
  * sla_verify, so both routes give bitwise equal states.

@@ -37,6 +37,12 @@ SLA_ROUTE_AUTO = 0
 SLA_ROUTE_SERIAL = 1
 SLA_ROUTE_PARALLEL = 2
 SLA_MAX_NODES = 64
+SLA_FAMILY_GDN = 0
+SLA_FAMILY_DELTANET = 1
+SLA_FAMILY_DECAY = 2
+SLA_FAMILY_GLA = 3
+FAMILIES = {"gdn": SLA_FAMILY_GDN, "deltanet": SLA_FAMILY_DELTANET, "decay": SLA_FAMILY_DECAY,
+            "gla": SLA_FAMILY_GLA}
 SLA_ACT_NONE = 0
 SLA_ACT_SILU = 1
 SLA_CONV_MAX_KERNEL = 4
@@ -48,7 +54,7 @@ TOPOLOGIES = {"tree": SLA_TOPO_TREE, "chain": SLA_TOPO_CHAIN}
 class SlaShape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("d_k", ctypes.c_int32),
                 ("d_v", ctypes.c_int32), ("n_nodes", ctypes.c_int32), ("qkv_dtype", ctypes.c_int32),
-                ("topology", ctypes.c_int32)]
+                ("topology", ctypes.c_int32), ("family", ctypes.c_int32)]
 
 
 class SlaFactors(ctypes.Structure):
@@ -150,9 +156,15 @@ def sla_validate_path_host(parent, path, length) -> int:
     return lib().sla_validate_path_host(p.ctypes.data, len(p), pa.ctypes.data, int(length))
 
 
-def make_shape(batch, heads, d_k, d_v, n_nodes, dtype="bf16", topology="tree") -> SlaShape:
+def make_shape(batch, heads, d_k, d_v, n_nodes, dtype="bf16", topology="tree", family="gdn") -> SlaShape:
     return SlaShape(int(batch), int(heads), int(d_k), int(d_v), int(n_nodes),
-                    SLA_DTYPE_BF16 if dtype == "bf16" else SLA_DTYPE_F32, TOPOLOGIES[topology])
+                    SLA_DTYPE_BF16 if dtype == "bf16" else SLA_DTYPE_F32, TOPOLOGIES[topology],
+                    FAMILIES[family])
+
+
+def gate_shape(batch, n, heads, d_k, family="gdn") -> tuple:
+    """Shape of the gate input and of the gate factor record for a family."""
+    return (batch, n, heads, d_k) if family == "gla" else (batch, n, heads)
 
 
 def sla_factors_bytes(shape: SlaShape) -> int:
@@ -198,22 +210,22 @@ class Factors:
     """A factor store (see sla_factors in include/sla.h) as torch tensors."""
     k: object       # [B][n][H][dk] activation dtype
     u: object       # [B][n][H][dv] fp32
-    alpha: object   # [B][n][H] fp32
+    alpha: object   # [B][n][H] fp32 gate ([B][n][H][dk] for GLA)
     parent: object  # [B][n] int32
 
     @staticmethod
-    def empty(batch, n, heads, d_k, d_v, dtype, device="cuda"):
+    def empty(batch, n, heads, d_k, d_v, dtype, device="cuda", family="gdn"):
         torch = _torch()
         return Factors(torch.empty(batch, n, heads, d_k, dtype=dtype, device=device),
                        torch.empty(batch, n, heads, d_v, dtype=torch.float32, device=device),
-                       torch.empty(batch, n, heads, dtype=torch.float32, device=device),
+                       torch.empty(gate_shape(batch, n, heads, d_k, family), dtype=torch.float32, device=device),
                        torch.empty(batch, n, dtype=torch.int32, device=device))
 
-    def c(self, dtype, B, n, H, dk, dv) -> SlaFactors:
+    def c(self, dtype, B, n, H, dk, dv, family="gdn") -> SlaFactors:
         torch = _torch()
         return SlaFactors(_dev(self.k, dtype, (B, n, H, dk), "factors.k"),
                           _dev(self.u, torch.float32, (B, n, H, dv), "factors.u"),
-                          _dev(self.alpha, torch.float32, (B, n, H), "factors.alpha"),
+                          _dev(self.alpha, torch.float32, gate_shape(B, n, H, dk, family), "factors.alpha"),
                           _dev(self.parent, torch.int32, (B, n), "factors.parent"))
 
 
@@ -224,22 +236,24 @@ def _check(code, what):
 
 def sla_verify(state, q, k, v, alpha, beta, parent_idx, out, factors: Factors, *,
                pending: Optional[tuple] = None, status=None, topology: str = "tree",
-               route: str = "auto"):
+               route: str = "auto", family: str = "gdn"):
     """Enqueue one verification on the current stream (see sla_verify in sla.h).
 
+    alpha: [B][n][H] fp32 ([B][n][H][dk] per-key gates for "gla"; None for
+    "deltanet"); beta: [B][n][H] fp32 (None for "decay" and "gla").
     pending: None or (factors_prev: Factors, path [B][n_prev] int32, len [B] int32).
     Raises SlaError on a host-detected error."""
     torch = _torch()
     B, n, H, dk = q.shape
     dv = v.shape[-1]
     dt = _dtype_code(q)
-    shape = SlaShape(B, H, dk, dv, n, dt, TOPOLOGIES[topology])
-    f = factors.c(q.dtype, B, n, H, dk, dv)
+    shape = SlaShape(B, H, dk, dv, n, dt, TOPOLOGIES[topology], FAMILIES[family])
+    f = factors.c(q.dtype, B, n, H, dk, dv, family)
     pend_p = None
     if pending is not None:
         pf, ppath, plen = pending
         pn = pf.parent.shape[1]
-        pend = SlaPending(pf.c(q.dtype, B, pn, H, dk, dv), pn,
+        pend = SlaPending(pf.c(q.dtype, B, pn, H, dk, dv, family), pn,
                           _dev(ppath, torch.int32, (B, pn), "pending.path"),
                           _dev(plen, torch.int32, (B,), "pending.len"))
         pend_p = ctypes.byref(pend)
@@ -247,19 +261,21 @@ def sla_verify(state, q, k, v, alpha, beta, parent_idx, out, factors: Factors, *
     code = lib().sla_verify(
         ctypes.byref(shape), ROUTES[route], _dev(state, torch.float32, (B, H, dk, dv), "state"), pend_p,
         _dev(q, q.dtype, (B, n, H, dk), "q"), _dev(k, q.dtype, (B, n, H, dk), "k"),
-        _dev(v, q.dtype, (B, n, H, dv), "v"), _dev(alpha, torch.float32, (B, n, H), "alpha"),
-        _dev(beta, torch.float32, (B, n, H), "beta"), _dev(parent_idx, torch.int32, (B, n), "parent_idx"),
+        _dev(v, q.dtype, (B, n, H, dv), "v"),
+        _dev(alpha, torch.float32, gate_shape(B, n, H, dk, family), "alpha") if alpha is not None else None,
+        _dev(beta, torch.float32, (B, n, H), "beta") if beta is not None else None,
+        _dev(parent_idx, torch.int32, (B, n), "parent_idx"),
         _dev(out, torch.float32, (B, n, H, dv), "out"), ctypes.byref(f), st_p, _stream(q.device))
     _check(code, "sla_verify")
 
 
-def sla_commit(state, factors: Factors, path, length, *, status=None):
+def sla_commit(state, factors: Factors, path, length, *, status=None, family: str = "gdn"):
     """Enqueue an immediate commit of the accepted paths (see sla_commit)."""
     torch = _torch()
     B, n, H, dk = factors.k.shape
     dv = factors.u.shape[-1]
-    shape = SlaShape(B, H, dk, dv, n, _dtype_code(factors.k), SLA_TOPO_TREE)
-    f = factors.c(factors.k.dtype, B, n, H, dk, dv)
+    shape = SlaShape(B, H, dk, dv, n, _dtype_code(factors.k), SLA_TOPO_TREE, FAMILIES[family])
+    f = factors.c(factors.k.dtype, B, n, H, dk, dv, family)
     st_p = _dev(status, torch.int32, (B,), "status") if status is not None else None
     code = lib().sla_commit(ctypes.byref(shape), _dev(state, torch.float32, (B, H, dk, dv), "state"),
                             ctypes.byref(f), _dev(path, torch.int32, (B, n), "path"),

@@ -39,6 +39,7 @@ int check_shape(const sla_shape *s) {
   if (s->d_k < 1 || s->d_v < 16 || s->d_v > 4096 || s->d_v % 16 != 0) return SLA_ERR_SHAPE;
   if (s->qkv_dtype != SLA_DTYPE_F32 && s->qkv_dtype != SLA_DTYPE_BF16) return SLA_ERR_DTYPE;
   if (s->topology != SLA_TOPO_TREE && s->topology != SLA_TOPO_CHAIN) return SLA_ERR_SHAPE;
+  if (s->family < SLA_FAMILY_GDN || s->family > SLA_FAMILY_GLA) return SLA_ERR_SHAPE;
   if (!dk_ok(s->d_k)) return SLA_ERR_UNSUPPORTED;
   // grid sizes stay far inside 2^31 workgroups
   if ((uint64_t)s->batch * (uint64_t)s->heads * (uint64_t)(s->d_v / 16) > (1ull << 30)) return SLA_ERR_SHAPE;
@@ -53,11 +54,18 @@ struct FactorSizes {
   size_t k, u, alpha, parent;
 };
 
+// gates per (b, j, h): one per key dimension for GLA, else one
+size_t gate_width(const sla_shape *s) { return s->family == SLA_FAMILY_GLA ? (size_t)s->d_k : 1; }
+
 FactorSizes factor_sizes(const sla_shape *s, int n) {
   const size_t bnh = (size_t)s->batch * n * s->heads;
   return FactorSizes{bnh * s->d_k * act_bytes(s->qkv_dtype), bnh * s->d_v * sizeof(float),
-                     bnh * sizeof(float), (size_t)s->batch * n * sizeof(int32_t)};
+                     bnh * gate_width(s) * sizeof(float), (size_t)s->batch * n * sizeof(int32_t)};
 }
+
+// which inputs the family's step reads
+bool reads_alpha(int family) { return family != SLA_FAMILY_DELTANET; }
+bool reads_beta(int family) { return family == SLA_FAMILY_GDN || family == SLA_FAMILY_DELTANET; }
 
 bool factors_complete(const sla_factors *f) { return f && f->k && f->u && f->alpha && f->parent; }
 
@@ -108,7 +116,9 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
                hipStream_t stream) {
   int st = check_shape(shape);
   if (st != SLA_OK) return st;
-  if (!state || !q || !k || !v || !alpha || !beta || !parent_idx || !out || !factors_complete(factors))
+  const int fam = shape->family;
+  if (!state || !q || !k || !v || (reads_alpha(fam) && !alpha) || (reads_beta(fam) && !beta) || !parent_idx ||
+      !out || !factors_complete(factors))
     return SLA_ERR_NULL;
   if (route != SLA_ROUTE_AUTO && route != SLA_ROUTE_SERIAL && route != SLA_ROUTE_PARALLEL) return SLA_ERR_SHAPE;
   if (pending) {
@@ -124,15 +134,21 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
       for (const Range &y : ins)
         if (overlaps(x, y)) return SLA_ERR_ALIAS;
     if (!aligned16(pending->f.k) || !aligned16(pending->f.u)) return SLA_ERR_UNSUPPORTED;
+    if (fam == SLA_FAMILY_GLA && !aligned16(pending->f.alpha)) return SLA_ERR_UNSUPPORTED;
   }
   if (!aligned16(state) || !aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(out) ||
       !aligned16(factors->k) || !aligned16(factors->u))
     return SLA_ERR_UNSUPPORTED;
+  if (fam == SLA_FAMILY_GLA && (!aligned16(alpha) || !aligned16(factors->alpha))) return SLA_ERR_UNSUPPORTED;
 
   const bool chain = shape->topology == SLA_TOPO_CHAIN;
   bool use_parallel;
+  // the tree-masked contraction takes scalar gates only: GLA's per-key gates
+  // stay on the serial route
+  const bool parallel_ok = fam != SLA_FAMILY_GLA &&
+                           sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype);
   if (route == SLA_ROUTE_PARALLEL) {
-    if (!sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype)) return SLA_ERR_UNSUPPORTED;
+    if (!parallel_ok) return SLA_ERR_UNSUPPORTED;
     use_parallel = true;
   } else if (route == SLA_ROUTE_SERIAL) {
     use_parallel = false;
@@ -140,7 +156,7 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
     // bf16 drafts, chains included, go to the tree-masked contraction on the
     // matrix cores (its one dense contraction streams the state better than
     // per-node reductions do); fp32 activations stay on the serial route.
-    use_parallel = sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype);
+    use_parallel = parallel_ok;
   }
 
   sla::VerifyArgs a;
@@ -151,6 +167,7 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
   a.dv = shape->d_v;
   a.n = shape->n_nodes;
   a.chain = chain;
+  a.family = fam;
   a.has_pending = pending != nullptr;
   a.state = state;
   if (pending) {
@@ -186,12 +203,14 @@ int sla_commit(const sla_shape *shape, float *state, const sla_factors *factors,
   if (st != SLA_OK) return st;
   if (!state || !factors_complete(factors) || !path || !len) return SLA_ERR_NULL;
   if (!aligned16(state) || !aligned16(factors->u)) return SLA_ERR_UNSUPPORTED;
+  if (shape->family == SLA_FAMILY_GLA && !aligned16(factors->alpha)) return SLA_ERR_UNSUPPORTED;
   sla::CommitArgs a;
   a.B = shape->batch;
   a.H = shape->heads;
   a.dk = shape->d_k;
   a.dv = shape->d_v;
   a.n = shape->n_nodes;
+  a.gate_vec = shape->family == SLA_FAMILY_GLA;
   a.state = state;
   a.k = factors->k;
   a.u = factors->u;

@@ -3,9 +3,10 @@
 //
 // Commit streams each unit's fp32 state once in and once out and applies the
 // accepted path's factor records in path order,
-//     H[i][c] <- alpha_a H[i][c] + k_a[i] u_a[c]     (a = path[0], path[1], ...)
-// through the same rank-one expression as the fused prologue of verification,
-// so the two routes produce bitwise equal states.
+//     H[i][c] <- g_a[i] H[i][c] + k_a[i] u_a[c]     (a = path[0], path[1], ...)
+// with g_a[i] = alpha_a for the scalar-gate families and the per-key gate of
+// GLA, through the same rank-one expression as the fused prologue of
+// verification, so the two routes produce bitwise equal states.
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -23,13 +24,15 @@ constexpr int kCommitStage = 8;   // path records staged in LDS; longer paths re
 // parent row and the gates whole (validation takes no dependent read), then
 // gathers the records the path names straight into LDS.  An invalid path
 // reports its status and leaves the state untouched.
-template <typename T, int DK>
+// VG: the records hold d_k gates each (GLA), staged like the key rows.
+template <typename T, int DK, bool VG>
 __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a) {
   constexpr int R = DK / 16;  // float4 groups per thread
   __shared__ int s_err, s_len;
   __shared__ float s_alpha[kCommitStage];
   __shared__ __attribute__((aligned(16))) unsigned char s_kraw[kCommitStage * DK * sizeof(T)];
   __shared__ __attribute__((aligned(16))) float s_u[kCommitStage][kCommitCols];
+  __shared__ __attribute__((aligned(16))) float s_g[VG ? kCommitStage * DK : 4];  // [kCommitStage][DK]
   const T *s_k = reinterpret_cast<const T *>(s_kraw);  // [kCommitStage][DK]
   const int tid = threadIdx.x;
   const int w = tid / kWave, l = tid % kWave;
@@ -49,7 +52,7 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a) {
     len = a.len[b];
     node = l < n ? a.path[rowp + l] : -1;
     par = l < n ? a.parent[rowp + l] : -2;
-    al = l < n ? a.alpha[(rowp + l) * H + h] : 0.f;
+    if (!VG) al = l < n ? a.alpha[(rowp + l) * H + h] : 0.f;
   }
   // the slab, before the path is known
   const int cg = slab * kCommitCols + (tid % 16) * 4;  // first column of this thread's float4
@@ -81,13 +84,20 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a) {
     const T *fk = static_cast<const T *>(a.k);
     constexpr int KC = DK * (int)sizeof(T) / 16;  // 16-byte chunks per key row
     constexpr int KI = kCommitStage * KC / kWave;
-    int nt[KI];  // shuffles first: an LDS instruction after an LDS-DMA load waits for it
+    constexpr int GC = DK * 4 / 16;  // 16-byte chunks per gate row
+    constexpr int GI = VG ? kCommitStage * GC / kWave : 0;
+    int nt[KI], ng[GI > 0 ? GI : 1];  // shuffles first: an LDS instruction after an LDS-DMA load waits for it
 #pragma unroll
     for (int i = 0; i < KI; ++i) nt[i] = __shfl(nodec, (i * kWave + l) / KC);
+#pragma unroll
+    for (int i = 0; i < GI; ++i) ng[i] = __shfl(nodec, (i * kWave + l) / GC);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < KI; ++i)
       load_lds16(fk + ((rowp + nt[i]) * H + h) * DK + ((i * kWave + l) % KC) * (16 / sizeof(T)), s_kraw + i * kWave * 16);
+#pragma unroll
+    for (int i = 0; i < GI; ++i)
+      load_lds16(a.alpha + ((rowp + ng[i]) * H + h) * DK + ((i * kWave + l) % GC) * 4, s_g + i * kWave * 4);
 #pragma unroll
     for (int t = 0; t < kCommitStage; ++t) {
       const int ntt = __builtin_amdgcn_readlane(nodec, t);
@@ -104,7 +114,7 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a) {
   for (int r = 0; r < R; ++r) {
     const int i = tid / 16 + 16 * r;
     for (int t = 0; t < len && t < kCommitStage; ++t) {
-      const float alt = s_alpha[t];
+      const float alt = VG ? s_g[t * DK + i] : s_alpha[t];
       const float ki = to_f32(s_k[t * DK + i]);
       const float4 u = *reinterpret_cast<const float4 *>(&s_u[t][cs]);
       x[r].x = apply_factor(x[r].x, alt, ki, u.x);
@@ -115,7 +125,7 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a) {
     // paths longer than the stage read their records directly
     for (int t = kCommitStage; t < len; ++t) {
       const size_t s = (rowp + a.path[rowp + t]) * H + h;
-      const float alt = a.alpha[s];
+      const float alt = VG ? a.alpha[s * DK + i] : a.alpha[s];
       const float ki = to_f32(static_cast<const T *>(a.k)[s * DK + i]);
       const float4 u = *reinterpret_cast<const float4 *>(a.u + s * dv + cg);
       x[r].x = apply_factor(x[r].x, alt, ki, u.x);
@@ -146,7 +156,7 @@ __global__ __launch_bounds__(kWave) void topology_kernel(TopologyArgs a) {
 
 template <typename T, int DK>
 hipError_t launch_commit_dk(const CommitArgs &a, hipStream_t s) {
-  auto kern = commit_kernel<T, DK>;
+  auto kern = a.gate_vec ? commit_kernel<T, DK, true> : commit_kernel<T, DK, false>;
   const dim3 grid((unsigned)((size_t)a.B * a.H * ((a.dv + kCommitCols - 1) / kCommitCols)));
   hipLaunchKernelGGL(kern, grid, dim3(kCommitThreads), 0, s, a);
   return hipGetLastError();

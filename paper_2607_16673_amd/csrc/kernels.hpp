@@ -11,7 +11,7 @@ namespace sla {
 struct PendingArgs {
   const void *k;          // [B][np][H][dk] activation dtype
   const float *u;         // [B][np][H][dv]
-  const float *alpha;     // [B][np][H]
+  const float *alpha;     // [B][np][H] ([B][np][H][dk]: per-key gates)
   const int32_t *parent;  // [B][np]
   int32_t n;              // np
   const int32_t *path;    // [B][np]
@@ -20,6 +20,7 @@ struct PendingArgs {
 
 struct VerifyArgs {
   int32_t B, H, dk, dv, n;
+  int32_t family;   // SLA_FAMILY_*: which of alpha, beta the step reads, and the gate layout
   bool chain;
   bool has_pending;
   bool late_state;  // parallel route: issue the state reads after the first barrier
@@ -39,6 +40,7 @@ struct VerifyArgs {
 
 struct CommitArgs {
   int32_t B, H, dk, dv, n;
+  bool gate_vec;  // alpha holds dk gates per record (GLA) instead of one
   float *state;
   const void *k;
   const float *u;

@@ -14,8 +14,12 @@
 //     H_j = alpha_j H_par + k_j u_j^T   (only if j has children)
 // which is the GDN step S_j = alpha_j S_par (I - beta_j k_j k_j^T) +
 // beta_j v_j k_j^T rewritten around the corrected value u_j (the factor
-// record stored for commit).  Nodes are visited in DFS pre-order; a chain
-// therefore advances the registers in place.  When the next node's parent is
+// record stored for commit).  The other layer families take the same loop:
+// DeltaNet with alpha = 1; the no-delta families (scalar decay, GLA) with
+// u_j = v_j; GLA's per-key gates g_j scale row i by g_j[i] in place of
+// alpha_j, so b_j = H_par^T (g_j * q_j) and H_j = diag(g_j) H_par + k_j u_j^T.
+// Nodes are visited in DFS pre-order; a chain therefore advances the
+// registers in place.  When the next node's parent is
 // not the state in registers (a branch point of a tree), that state is
 // rebuilt from the committed tile kept in registers by re-applying the
 // stored factors of the parent's root path -- rank-one updates only, the
@@ -29,7 +33,8 @@ namespace {
 constexpr int kCols = 16;
 constexpr int kGroups = kWave / kCols;
 
-template <int DK, typename T, bool CHAIN>
+// VG: per-key gates (GLA), staged on chip like the keys.
+template <int DK, typename T, bool CHAIN, bool VG>
 __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   constexpr int R = DK / kGroups;
   const int lane = threadIdx.x;
@@ -45,6 +50,8 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   const int col = tile * kCols + c;
   const int row0 = g * R;
   const size_t unit = (size_t)b * H + h;
+  // delta-rule families correct the value against the parent state
+  const bool delta = a.family == SLA_FAMILY_GDN || a.family == SLA_FAMILY_DELTANET;
 
   // The state tile: the only state read of this call.
   float *st = a.state + unit * DK * dv + col;
@@ -68,7 +75,8 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   extern __shared__ float lds[];
   float *ks = lds;                   // [n][DK]
   float *qs = ks + n * DK;           // [n][DK]
-  float *vs = qs + n * DK;           // [n][kCols]
+  float *gs = qs + n * DK;           // [n][DK] per-key gates (VG only)
+  float *vs = gs + (VG ? n * DK : 0);  // [n][kCols]
   float *us = vs + n * kCols;        // [n][kCols]
   float *als = us + n * kCols;       // [n]
   float *bes = als + n;              // [n]
@@ -85,6 +93,7 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
     const size_t src = (((size_t)b * n + j) * H + h) * DK + i;
     ks[idx] = to_f32(k[src]);
     qs[idx] = to_f32(q[src]);
+    if (VG) gs[idx] = a.alpha[src];
   }
   for (int idx = lane; idx < n * kCols; idx += kWave) {
     const int j = idx / kCols, cc = idx % kCols;
@@ -92,24 +101,26 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   }
   if (lane < n) {
     const size_t s = ((size_t)b * n + lane) * H + h;
-    als[lane] = a.alpha[s];
-    bes[lane] = a.beta[s];
+    als[lane] = (VG || a.family == SLA_FAMILY_DELTANET) ? 1.f : a.alpha[s];
+    bes[lane] = delta ? a.beta[s] : 0.f;
     ords[topo.pos] = lane;
     pars[lane] = topo.parent;
     kids[lane] = topo.n_children;
     ancs[lane] = topo.anc;
   }
   // Factor records that do not depend on the V-tile: written once per unit
-  // (k, alpha) and once per sequence (parent).
+  // (k, gate) and once per sequence (parent).
   if (tile == 0) {
     T *fk = static_cast<T *>(a.fk);
     for (int idx = lane; idx < n * DK; idx += kWave) {
       const int j = idx / DK, i = idx % DK;
       const size_t s = (((size_t)b * n + j) * H + h) * DK + i;
       fk[s] = k[s];
+      if (VG) a.falpha[s] = a.alpha[s];
     }
     if (lane < n) {
-      a.falpha[((size_t)b * n + lane) * H + h] = a.alpha[((size_t)b * n + lane) * H + h];
+      const size_t s = ((size_t)b * n + lane) * H + h;
+      if (!VG) a.falpha[s] = a.family == SLA_FAMILY_DELTANET ? 1.f : a.alpha[s];
       if (h == 0) a.fparent[(size_t)b * n + lane] = topo.parent;
     }
   }
@@ -123,12 +134,18 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
     for (int t = 0; t < plen; ++t) {
       const int node = a.pend.path[(size_t)b * pn + t];
       const size_t s = ((size_t)b * pn + node) * H + h;
-      const float al = a.pend.alpha[s];
       const float u = a.pend.u[s * dv + col];
-      float kr[R];
+      float kr[R], gr[R];
       load_f32<R>(pk + s * DK + row0, kr);
+      if (VG) {
+        load_f32<R>(a.pend.alpha + s * DK + row0, gr);
+      } else {
+        const float al = a.pend.alpha[s];
 #pragma unroll
-      for (int r = 0; r < R; ++r) H0[r] = apply_factor(H0[r], al, kr[r], u);
+        for (int r = 0; r < R; ++r) gr[r] = al;
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) H0[r] = apply_factor(H0[r], gr[r], kr[r], u);
     }
 #pragma unroll
     for (int r = 0; r < R; ++r) st[(size_t)(row0 + r) * dv] = H0[r];
@@ -153,19 +170,21 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
           const float al = als[x];
           const float u = us[x * kCols + c];
           const float *kx = ks + x * DK + row0;
+          const float *gx = gs + x * DK + row0;
 #pragma unroll
-          for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], al, kx[r], u);
+          for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], VG ? gx[r] : al, kx[r], u);
         }
       }
     }
     const float *kj = ks + j * DK + row0;
     const float *qj = qs + j * DK + row0;
+    const float *gj = gs + j * DK + row0;
     float sk = 0.f, sq = 0.f, kq = 0.f;
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const float kr = kj[r], qr = qj[r];
       sk = __builtin_fmaf(Hc[r], kr, sk);
-      sq = __builtin_fmaf(Hc[r], qr, sq);
+      sq = __builtin_fmaf(Hc[r], VG ? gj[r] * qr : qr, sq);
       kq = __builtin_fmaf(kr, qr, kq);
     }
     sk += __shfl_xor(sk, 16);
@@ -175,7 +194,7 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
     sq += __shfl_xor(sq, 32);
     kq += __shfl_xor(kq, 32);
     const float al = als[j], be = bes[j];
-    const float u = be * (vs[j * kCols + c] - al * sk);
+    const float u = delta ? be * (vs[j * kCols + c] - al * sk) : vs[j * kCols + c];
     const float o = __builtin_fmaf(kq, u, al * sq);
     if (g == 0) {
       const size_t s = ((size_t)b * n + j) * H + h;
@@ -186,7 +205,7 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
     const bool internal = CHAIN ? (t + 1 < n) : (kids[j] > 0);
     if (internal) {
 #pragma unroll
-      for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], al, kj[r], u);
+      for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], VG ? gj[r] : al, kj[r], u);
       cur = j;
     } else {
       cur = p;
@@ -194,8 +213,8 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   }
 }
 
-size_t serial_lds_bytes(int n, int dk) {
-  return sizeof(float) * ((size_t)2 * n * dk + 2 * n * kCols + 2 * n) + sizeof(int) * (3 * n + (n & 1)) +
+size_t serial_lds_bytes(int n, int dk, bool vg) {
+  return sizeof(float) * ((size_t)(vg ? 3 : 2) * n * dk + 2 * n * kCols + 2 * n) + sizeof(int) * (3 * n + (n & 1)) +
          sizeof(uint64_t) * n;
 }
 
@@ -219,9 +238,14 @@ hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const
 template <int DK, typename T>
 hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
   const dim3 grid((unsigned)((size_t)a.B * a.H * (a.dv / kCols)));
-  const size_t lds = serial_lds_bytes(a.n, DK);
-  if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true>, grid, lds, s, a);
-  return launch_with_lds(verify_serial_kernel<DK, T, false>, grid, lds, s, a);
+  const bool vg = a.family == SLA_FAMILY_GLA;
+  const size_t lds = serial_lds_bytes(a.n, DK, vg);
+  if (vg) {
+    if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true, true>, grid, lds, s, a);
+    return launch_with_lds(verify_serial_kernel<DK, T, false, true>, grid, lds, s, a);
+  }
+  if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true, false>, grid, lds, s, a);
+  return launch_with_lds(verify_serial_kernel<DK, T, false, false>, grid, lds, s, a);
 }
 
 template <typename T>

@@ -129,7 +129,9 @@ __device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x
 template <int DK, int NP, int TPW>
 constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
 
-template <int DK, int NP, int CW, int TPW>
+// DELTA: the delta-rule families (GDN, DeltaNet).  Without the delta rule
+// (scalar decay) Lk = 0, so T = I and U = R = V: no P_k, no Lk, no T.
+template <int DK, int NP, int CW, int TPW, bool DELTA>
 __global__ __launch_bounds__((CW + 1) * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
 void verify_tile_kernel(VerifyArgs a) {
   using L = Layout<DK, NP, CW, TPW>;
@@ -226,8 +228,8 @@ void verify_tile_kernel(VerifyArgs a) {
     const bool live = l < n;
     const size_t s = (nbase + (live ? l : 0)) * H + h;
     p = live ? a.parent[nbase + l] : -1;
-    al = live ? a.alpha[s] : 1.f;
-    const float be = live ? a.beta[s] : 0.f;
+    al = (live && a.family != SLA_FAMILY_DELTANET) ? a.alpha[s] : 1.f;  // DeltaNet: no decay
+    const float be = (DELTA && live) ? a.beta[s] : 0.f;
     // pending accepted path, with the previous round's parent row and gates
     // read whole, so that validating the path waits on no further read
     int plen = 0, node = -1, prow_parent = -2;
@@ -360,7 +362,7 @@ void verify_tile_kernel(VerifyArgs a) {
     for (int mr = 0; mr < MT; ++mr)
 #pragma unroll
       for (int na = 0; na <= mr % NT; ++na, ++tc) {
-        if (tc % kColWaves != w || (mr % NT) * 16 >= n) continue;
+        if (tc % kColWaves != w || (mr % NT) * 16 >= n || (!DELTA && mr >= NT)) continue;
         f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -375,7 +377,7 @@ void verify_tile_kernel(VerifyArgs a) {
     for (int mr = 0; mr < MT; ++mr)
 #pragma unroll
       for (int na = 0; na <= mr % NT; ++na, ++tc) {
-        if (tc % kColWaves != w || (mr % NT) * 16 >= n) continue;
+        if (tc % kColWaves != w || (mr % NT) * 16 >= n || (!DELTA && mr >= NT)) continue;
         // every LDS read of the tile's metadata is issued before its first
         // write, so they share one round trip
         const int an = na * 16 + lc;
@@ -410,7 +412,7 @@ void verify_tile_kernel(VerifyArgs a) {
   if (w == kSetup) __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // the gathered records have landed
   __syncthreads();
 
-  if (w == kSetup) {
+  if (DELTA && w == kSetup) {
     // ---- T = (I + Lk)^-1, one lane per row j.  With p_0 .. p_{d-1} = j the
     //      root path of j and x_t = T_{j p_t}:  x_{d-1} = 1,
     //      x_t = - sum_{u > t} x_u Lk_{p_u p_t}.
@@ -543,15 +545,17 @@ void verify_tile_kernel(VerifyArgs a) {
       f32x4 pk[NT];
 #pragma unroll
       for (int mt = 0; mt < NT; ++mt) pk[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if constexpr (DELTA) {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 bhi, blo;
-        split8(hf[ks], bhi, blo);
+        for (int ks = 0; ks < KS; ++ks) {
+          bf16x8 bhi, blo;
+          split8(hf[ks], bhi, blo);
 #pragma unroll
-        for (int mt = 0; mt < NT; ++mt) {
-          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + mt * 16 + lc, ks * 4 + lg));
-          pk[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pk[mt], 0, 0, 0);
-          pk[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pk[mt], 0, 0, 0);
+          for (int mt = 0; mt < NT; ++mt) {
+            const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + mt * 16 + lc, ks * 4 + lg));
+            pk[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pk[mt], 0, 0, 0);
+            pk[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pk[mt], 0, 0, 0);
+          }
         }
       }
       // R in the accumulator layout (the row base is rebuilt per tile:
@@ -565,7 +569,8 @@ void verify_tile_kernel(VerifyArgs a) {
           const int j = mt * 16 + rb + q;
           uint32_t vb = vraw[mt][q];
           __asm__("" : "+v"(vb));  // keeps the widening here, not next to the load
-          rreg[mt][q] = j < n ? s_be[j] * (__uint_as_float(vb << 16) - s_gamma[j] * pk[mt][q]) : 0.f;
+          const float vf = __uint_as_float(vb << 16);
+          rreg[mt][q] = j < n ? (DELTA ? s_be[j] * (vf - s_gamma[j] * pk[mt][q]) : vf) : 0.f;
         }
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -604,20 +609,25 @@ void verify_tile_kernel(VerifyArgs a) {
     if (cols_live) {  // no early return: every wave takes every later barrier
       // ---- U = T R, then O = Gamma P_q + Attn U, on the matrix cores; A
       //      fragments are rows j = 16 mt + lc, columns 16 ks + 4 lg .. + 3
-      s16x4 rhi[NT], rlo[NT];
+      f32x4 uacc[NT];  // same layout as R
+      if constexpr (DELTA) {
+        s16x4 rhi[NT], rlo[NT];
 #pragma unroll
-      for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
-      f32x4 uacc[NT];
+        for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
 #pragma unroll
-      for (int mt = 0; mt < NT; ++mt) {
-        uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int mt = 0; mt < NT; ++mt) {
+          uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int ks = 0; ks <= mt; ++ks) {
-          const f32x4 tv = *reinterpret_cast<const f32x4 *>(tb + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
-          s16x4 th, tlo;
-          split4(tv, th, tlo);
-          uacc[mt] = mfma16_split(th, tlo, rhi[ks], rlo[ks], uacc[mt]);
+          for (int ks = 0; ks <= mt; ++ks) {
+            const f32x4 tv = *reinterpret_cast<const f32x4 *>(tb + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
+            s16x4 th, tlo;
+            split4(tv, th, tlo);
+            uacc[mt] = mfma16_split(th, tlo, rhi[ks], rlo[ks], uacc[mt]);
+          }
         }
+      } else {
+#pragma unroll
+        for (int mt = 0; mt < NT; ++mt) uacc[mt] = rreg[mt];
       }
       s16x4 uhi[NT], ulo[NT];
 #pragma unroll
@@ -674,12 +684,12 @@ int device_cus() {
 // hold them back briefly instead (stagger).
 constexpr int kLateRounds = 4;
 
-template <int DK, int NP, int CW, int TPW>
-hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
+template <int DK, int NP, int CW, int TPW, bool DELTA>
+hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
   using L = Layout<DK, NP, CW, TPW>;
   const size_t lds = L::kBytes;
   if (lds > kMaxLds) return hipErrorInvalidConfiguration;
-  auto kern = verify_tile_kernel<DK, NP, CW, TPW>;
+  auto kern = verify_tile_kernel<DK, NP, CW, TPW, DELTA>;
   if (lds > kDefaultLds) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -699,6 +709,12 @@ hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
   b.stagger = !b.late_state && groups >= slots;
   hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3((CW + 1) * kWave), lds, s, b);
   return hipGetLastError();
+}
+
+template <int DK, int NP, int CW, int TPW>
+hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
+  if (a.family == SLA_FAMILY_DECAY) return launch_np_fam<DK, NP, CW, TPW, false>(a, s);
+  return launch_np_fam<DK, NP, CW, TPW, true>(a, s);
 }
 
 template <int DK>

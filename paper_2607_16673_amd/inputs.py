@@ -12,6 +12,10 @@ proposal trees of the paper's evaluation, §8, which are not available):
     rounded (round-to-nearest-even) to the activation dtype;
   * v ~ N(0, 1), rounded to the activation dtype;
   * alpha = sigmoid(x), x ~ U(2, 5); beta = sigmoid(z), z ~ N(0, 1); fp32;
+  * other layer families (the factor-record remark of §5.1): DeltaNet reads
+    beta only, the scalar-decay family alpha only (both as above); GLA's
+    per-key gates are g = sigmoid(z)^(1/16), z ~ N(0, 1) per (layer, b,
+    node, head, key dimension), fp32 (GLA's gate with its normaliser 16);
   * chains: parent[j] = j - 1; trees: node 0 is the root, node i > 0 picks a
     uniform parent among earlier nodes whose depth and child count are still
     below the configured limits;
@@ -203,6 +207,31 @@ def draw_layer(cfg: Config, layer: int, round_index: int = 0, batch: int | None 
     k, k32 = _to_dtype(k64, cfg.dtype)
     v, v32 = _to_dtype(v64, cfg.dtype)
     return dict(q=q, k=k, v=v, q32=q32, k32=k32, v32=v32, alpha=alpha, beta=beta)
+
+
+FAMILIES = ("gdn", "deltanet", "decay", "gla")
+
+
+def draw_gla_gates(cfg: Config, layer: int, round_index: int = 0, batch: int | None = None) -> np.ndarray:
+    """GLA per-key gates of one layer of one round, [B][n][H][dk] fp32."""
+    B = cfg.batch if batch is None else batch
+    rng = _rng(base_seed(cfg), round_index, 5, layer)
+    z = rng.standard_normal((B, cfg.n_nodes, cfg.heads, cfg.d_k))
+    return ((1.0 / (1.0 + np.exp(-z))) ** (1.0 / 16.0)).astype(np.float32)
+
+
+def family_gates(cfg: Config, rnd, layer_pos: int, family: str, layer: int | None = None,
+                 round_index: int = 0, batch: int | None = None):
+    """(alpha input, beta input) a family reads, None where it reads none."""
+    if family == "gdn":
+        return rnd.alpha[layer_pos], rnd.beta[layer_pos]
+    if family == "deltanet":
+        return None, rnd.beta[layer_pos]
+    if family == "decay":
+        return rnd.alpha[layer_pos], None
+    if family == "gla":
+        return draw_gla_gates(cfg, layer_pos if layer is None else layer, round_index, batch), None
+    raise ValueError(family)
 
 
 def draw_state(cfg: Config, layer: int, batch: int | None = None) -> np.ndarray:

@@ -167,6 +167,46 @@ def test_verify_rejects_pending_aliasing_output_factors():
                               None, None) == B.SLA_ERR_UNSUPPORTED
 
 
+def test_family_argument_rules_return_before_launch():
+    """Each family requires exactly the inputs its step reads.  A call whose
+    pointers pass the null checks is stopped by a misaligned state pointer, so
+    nothing is launched."""
+    L = B.lib()
+    f = B.SlaFactors(_ptr(10), _ptr(11), _ptr(12), _ptr(13))
+
+    def call(family, alpha, beta, state=None, route=0, shape=None):
+        s = shape or B.make_shape(2, 4, 128, 128, 8, "bf16", family=family)
+        args = [state or _ptr(0)] + [_ptr(i) for i in range(1, 9)]
+        args[4], args[5] = alpha, beta
+        return L.sla_verify(ctypes.byref(s), route, args[0], None, *args[1:8], ctypes.byref(f), None, None)
+
+    mis = ctypes.c_void_p(FAKE + 4)
+    # DeltaNet: beta required, alpha not read
+    assert call("deltanet", _ptr(4), None) == B.SLA_ERR_NULL
+    assert call("deltanet", None, _ptr(5), state=mis) == B.SLA_ERR_UNSUPPORTED
+    # no-delta families: alpha (gates) required, beta not read
+    for fam in ("decay", "gla"):
+        assert call(fam, None, _ptr(5)) == B.SLA_ERR_NULL
+        assert call(fam, _ptr(4), None, state=mis) == B.SLA_ERR_UNSUPPORTED
+    assert call("gdn", None, _ptr(5)) == B.SLA_ERR_NULL
+    assert call("gdn", _ptr(4), None) == B.SLA_ERR_NULL
+    # GLA's per-key gates run on the serial route only
+    assert call("gla", _ptr(4), None, route=B.SLA_ROUTE_PARALLEL) == B.SLA_ERR_UNSUPPORTED
+    assert call("gla", ctypes.c_void_p(FAKE + 4 * (1 << 24) + 4), None) == B.SLA_ERR_UNSUPPORTED  # gates misaligned
+    bad = B.make_shape(2, 4, 128, 128, 8, "bf16")
+    bad.family = 4
+    assert call("gdn", _ptr(4), _ptr(5), shape=bad) == B.SLA_ERR_SHAPE
+    assert L.sla_commit(ctypes.byref(bad), _ptr(0), ctypes.byref(f), _ptr(1), _ptr(2), None, None) == B.SLA_ERR_SHAPE
+
+
+def test_factor_store_bytes_per_family():
+    bnh = 2 * 8 * 4
+    base = bnh * 128 * 2 + bnh * 64 * 4 + 2 * 8 * 4
+    for fam in ("gdn", "deltanet", "decay"):
+        assert B.sla_factors_bytes(B.make_shape(2, 4, 128, 64, 8, "bf16", family=fam)) == base + bnh * 4
+    assert B.sla_factors_bytes(B.make_shape(2, 4, 128, 64, 8, "bf16", family="gla")) == base + bnh * 128 * 4
+
+
 def test_commit_and_topology_argument_errors():
     L = B.lib()
     ok = B.make_shape(2, 4, 128, 128, 8, "bf16")
