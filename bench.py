@@ -36,19 +36,22 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_bytes(cfg, pending_len):
+def algorithmic_bytes(cfg, pending_len, family="gdn"):
     """Bytes one fused verify call must move for one layer: the state once in
-    and once out, the draft's q/k/v/alpha/beta/parent, the outputs, the
-    factor store, and the pending records of the accepted paths."""
+    and once out, the draft's q/k/v, the gates and betas the layer family
+    reads, the parent row, the outputs, the factor store, and the pending
+    records of the accepted paths."""
     B, H, dk, dv, n = cfg.batch, cfg.heads, cfg.d_k, cfg.d_v, cfg.n_nodes
     w = 2 if cfg.dtype == "bf16" else 4
     bnh = B * n * H
+    gate = dk * 4 if family == "gla" else 4            # gate record (alpha, 1, or per-key gates)
+    gin = {"gdn": 8, "deltanet": 4, "decay": 4, "gla": dk * 4}[family]  # gate and beta inputs read
     state = 2 * B * H * dk * dv * 4
-    draft = bnh * (2 * dk * w + dv * w + 8) + B * n * 4
+    draft = bnh * (2 * dk * w + dv * w + gin) + B * n * 4
     out = bnh * dv * 4
-    factors = bnh * (dk * w + dv * 4 + 4) + B * n * 4
+    factors = bnh * (dk * w + dv * 4 + gate) + B * n * 4
     A = int(np.sum(pending_len))
-    pend = A * H * (dk * w + dv * 4 + 4) + A * 4 + B * 4 * 2 + B * n * 4
+    pend = A * H * (dk * w + dv * 4 + gate) + A * 4 + B * 4 * 2 + B * n * 4
     return state + draft + out + factors + pend
 
 
@@ -63,10 +66,11 @@ def graph_plan(steps, layers, max_launches=48):
     return g, k // g
 
 
-def cpu_baseline(cfg, rounds, states, budget_s=10.0):
+def cpu_baseline(cfg, rounds, states, budget_s=10.0, gates=None, family="gdn"):
     """The fp64 oracle (verify + commit by definition) on the host cores, on
     whole layers of the same workload, cycling through the layers until about
-    budget_s of CPU time has passed."""
+    budget_s of CPU time has passed.  gates: per layer (alpha, beta) inputs of
+    the family."""
     import oracle
 
     r0 = rounds
@@ -74,10 +78,11 @@ def cpu_baseline(cfg, rounds, states, budget_s=10.0):
     passes = 0
     while True:
         layer = passes % cfg.layers
-        out, st = oracle.verify(states[layer], r0.q32[layer], r0.k32[layer], r0.v32[layer], r0.alpha[layer],
-                                r0.beta[layer], r0.parent)
-        S1, st2 = oracle.commit(states[layer], r0.k32[layer], r0.v32[layer], r0.alpha[layer],
-                                r0.beta[layer], r0.parent, r0.path, r0.length)
+        a, b = gates[layer] if gates is not None else (r0.alpha[layer], r0.beta[layer])
+        out, st = oracle.verify(states[layer], r0.q32[layer], r0.k32[layer], r0.v32[layer], a, b, r0.parent,
+                                family=family)
+        S1, st2 = oracle.commit(states[layer], r0.k32[layer], r0.v32[layer], a, b, r0.parent, r0.path,
+                                r0.length, family=family)
         assert (st == 0).all() and (st2 == 0).all()
         passes += 1
         if time.perf_counter() - t0 >= budget_s:
@@ -97,6 +102,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--route", default="auto", choices=["auto", "serial", "parallel"])
+    ap.add_argument("--family", default="gdn", choices=["gdn", "deltanet", "decay", "gla"],
+                    help="layer family of the recurrent core (gdn: gated delta rule, the headline; deltanet: "
+                         "no decay; decay: scalar decay without the delta rule; gla: per-key gates)")
     ap.add_argument("--separate", action="store_true",
                     help="time the separate route (verify, then standalone commit) instead of the fused one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -151,17 +159,22 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
 
     adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    fam = args.family
+    gates = [inputs.family_gates(cfg, rnd, l, fam, layer=l) for l in range(cfg.layers)]
+
+    def dev_or_none(x):
+        return torch.from_numpy(x).to(dev) if x is not None else None
+
     layers = []
     for l in range(cfg.layers):
         layers.append(dict(q=act(rnd.q[l]), k=act(rnd.k[l]), v=act(rnd.v[l]),
-                           alpha=torch.from_numpy(rnd.alpha[l]).to(dev),
-                           beta=torch.from_numpy(rnd.beta[l]).to(dev)))
+                           alpha=dev_or_none(gates[l][0]), beta=dev_or_none(gates[l][1])))
     parent = torch.from_numpy(rnd.parent).to(dev)
     path = torch.from_numpy(rnd.path).to(dev)
     length = torch.from_numpy(rnd.length).to(dev)
     states = [torch.from_numpy(s).to(dev) for s in states_np]
     fshape = (cfg.batch, cfg.n_nodes, cfg.heads, cfg.d_k, cfg.d_v)
-    fstores = [[B.Factors.empty(*fshape, adt, dev) for _ in range(cfg.layers)] for _ in range(2)]
+    fstores = [[B.Factors.empty(*fshape, adt, dev, family=fam) for _ in range(cfg.layers)] for _ in range(2)]
     outs = [torch.empty(cfg.batch, cfg.n_nodes, cfg.heads, cfg.d_v, dtype=torch.float32, device=dev)
             for _ in range(cfg.layers)]
     status = torch.zeros(cfg.batch, dtype=torch.int32, device=dev)
@@ -179,15 +192,15 @@ def main():
                 events[-1].record(stream)
             if args.separate:
                 B.sla_verify(states[l], L["q"], L["k"], L["v"], L["alpha"], L["beta"], parent, outs[l], cur[l],
-                             status=status, topology=topo, route=args.route)
+                             status=status, topology=topo, route=args.route, family=fam)
                 if events is not None:
                     events.append(torch.cuda.Event(enable_timing=True))
                     events[-1].record(stream)
-                B.sla_commit(states[l], cur[l], path, length, status=status)
+                B.sla_commit(states[l], cur[l], path, length, status=status, family=fam)
             else:
                 pend = (prev[l], path, length) if s > 0 else None
                 B.sla_verify(states[l], L["q"], L["k"], L["v"], L["alpha"], L["beta"], parent, outs[l], cur[l],
-                             pending=pend, status=status, topology=topo, route=args.route)
+                             pending=pend, status=status, topology=topo, route=args.route, family=fam)
             if events is not None:
                 events.append(torch.cuda.Event(enable_timing=True))
                 events[-1].record(stream)
@@ -259,7 +272,7 @@ def main():
     # per layer: the fused call, or with --separate the verify (state read
     # once) plus the standalone commit (state read and written once more)
     v_ms = float(np.mean(vdur)) + (float(np.mean(cdur)) if cdur else 0.0)
-    bytes_launch = algorithmic_bytes(cfg, rnd.length)
+    bytes_launch = algorithmic_bytes(cfg, rnd.length, fam)
     if args.separate:
         bytes_launch += cfg.batch * cfg.heads * cfg.d_k * cfg.d_v * 4
     achieved = bytes_launch / (v_ms * 1e-3) / 1e9
@@ -271,6 +284,8 @@ def main():
         with open(args.traffic_json) as f:
             tj = json.load(f)
         key = "%s/%s/%s" % (cfg.name, args.route, "separate" if args.separate else "fused")
+        if fam != "gdn":
+            key += "/" + fam
         # counters taken on other library sources no longer describe this kernel
         from paper_2607_16673_amd.traffic import source_digest
         if key in tj and tj[key].get("source_sha256") == source_digest("gdn"):
@@ -288,7 +303,8 @@ def main():
                    "d_v": cfg.d_v, "nodes_per_tree": cfg.n_nodes, "topology": topo,
                    "max_depth": cfg.max_depth, "max_branch": cfg.max_branch, "layers": cfg.layers,
                    "qkv_dtype": cfg.dtype, "state_dtype": "f32", "route": args.route,
-                   "commit": "separate" if args.separate else "fused", "parallelism": "single-gpu",
+                   "commit": "separate" if args.separate else "fused", "family": fam,
+                   "parallelism": "single-gpu",
                    "launch": "hip graph" if args.graph else "eager"},
         "hbm_gbps": round(achieved, 1),
         # one token through every layer of the workload (one layer's node is `value`'s unit)
@@ -299,7 +315,7 @@ def main():
         line["commit_avg_launch_ms"] = round(float(np.mean(cdur)), 5)
     if not args.no_cpu_baseline:
         log("bench: oracle CPU baseline")
-        line["cpu_baseline"] = cpu_baseline(cfg, rnd, states_np)
+        line["cpu_baseline"] = cpu_baseline(cfg, rnd, states_np, gates=gates, family=fam)
     print(json.dumps(line), flush=True)
 
 

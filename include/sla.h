@@ -171,10 +171,13 @@ typedef struct sla_pending {
  *   out     device fp32 [B][n][H][d_v]; o_j = S_j q_j.
  *   factors device factor store written for this draft (see sla_factors).
  *   status  device int32 [B] or NULL: 0, SLA_ERR_TOPOLOGY or SLA_ERR_PATH.
- *   route   SLA_ROUTE_*.  GLA runs on the serial route only (PARALLEL:
- *           SLA_ERR_UNSUPPORTED; AUTO takes SERIAL), and the serial route
- *           stages k, q and the gates of all nodes on chip: for GLA at
- *           d_k = 256 that limits n to 50 (SLA_ERR_UNSUPPORTED above).
+ *   route   SLA_ROUTE_*.  Both routes stage the draft on chip.  With GLA's
+ *           per-key gates the parallel route holds d_k = 256 drafts of up
+ *           to 32 nodes (PARALLEL: SLA_ERR_UNSUPPORTED above; AUTO then takes
+ *           SERIAL), and the serial route d_k = 256 drafts of up to 50 nodes
+ *           (SLA_ERR_UNSUPPORTED above).  Gates (alpha, GLA's g) lie in
+ *           (0, 1]; the parallel route divides by their products along a
+ *           root path, which must stay within the fp32 normal range.
  * Returns SLA_OK once the work is enqueued, or a negative error code. */
 int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pending *pending,
                const void *q, const void *k, const void *v, const float *alpha,

@@ -143,10 +143,7 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
 
   const bool chain = shape->topology == SLA_TOPO_CHAIN;
   bool use_parallel;
-  // the tree-masked contraction takes scalar gates only: GLA's per-key gates
-  // stay on the serial route
-  const bool parallel_ok = fam != SLA_FAMILY_GLA &&
-                           sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype);
+  const bool parallel_ok = sla::parallel_supported(shape->d_k, shape->d_v, shape->n_nodes, shape->qkv_dtype);
   if (route == SLA_ROUTE_PARALLEL) {
     if (!parallel_ok) return SLA_ERR_UNSUPPORTED;
     use_parallel = true;
@@ -191,8 +188,13 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
   a.falpha = factors->alpha;
   a.fparent = factors->parent;
   a.status = status;
-  const hipError_t e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)
-                                    : sla::launch_verify_serial(a, shape->qkv_dtype, stream);
+  hipError_t e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)
+                              : sla::launch_verify_serial(a, shape->qkv_dtype, stream);
+  // a draft whose on-chip stage does not fit the contraction's LDS (GLA's
+  // per-key gates at the largest shapes) is refused before any launch; the
+  // automatic route then takes the serial one
+  if (e == hipErrorInvalidConfiguration && use_parallel && route == SLA_ROUTE_AUTO)
+    e = sla::launch_verify_serial(a, shape->qkv_dtype, stream);
   if (e == hipErrorInvalidConfiguration) return SLA_ERR_UNSUPPORTED;
   return hip_status(e);
 }

@@ -59,21 +59,37 @@ constexpr int kPMax = 8;                          // pending steps staged in LDS
 constexpr int kBP = 20;                           // fp32 row pitch of a 16x16 block
 constexpr int kZ = 8;                             // root paths up to this depth solve T in registers
 
-template <int DK, int NP, int CW, int TPW>
+// Layer families by the form of their step (template parameter KIND):
+//   kKindDelta  GDN and DeltaNet: the delta rule, scalar gate;
+//   kKindDecay  scalar decay without the delta rule: Lk = 0, T = I, U = V;
+//   kKindGates  GLA: one gate per key dimension, no delta rule.  The decay
+//               ratios become per-dimension, D_ja[i] = Gamma_j[i] / Gamma_a[i],
+//               and fold into the operands: Q~_j = Gamma_j * q_j and
+//               K~_a = k_a / Gamma_a (fp32, split into bf16 hi + lo), so
+//               Attn_ja = Q~_j . K~_a and O = Q~ H0 + Attn V.
+constexpr int kKindDelta = 0, kKindDecay = 1, kKindGates = 2;
+
+template <int DK, int NP, int CW, int TPW, int KIND>
 struct Layout {
   static constexpr int kTileCols = CW * kWaveCols;
   static constexpr int NT = NP / 16, KS = DK / 32, CH = DK / 8, MT = 2 * NT;
   static constexpr int NB = NT * (NT + 1) / 2;      // lower-triangular 16x16 blocks
   static constexpr int kList = NP * (NP + 1) / 2;   // compact Lk capacity (floats)
+  static constexpr bool kDelta = KIND == kKindDelta, kGates = KIND == kKindGates;
   static constexpr int kX = 2 * NP * CH * 16;       // [Q; K], 16-byte chunks, xor-swizzled
   static constexpr int kBlk = 16 * kBP * 4;
-  static constexpr int kT = NB * kBlk;              // T blocks
+  static constexpr int kT = kDelta ? NB * kBlk : 0;   // T blocks
   static constexpr int kAt = NB * kBlk;             // Attn blocks
-  static constexpr int kLk = kList * 4;
+  static constexpr int kLk = kDelta ? kList * 4 : 0;
   static constexpr int kPk = kPMax * DK * 2;        // pending keys (bf16)
   static constexpr int kPu = TPW * kPMax * kTileCols * 4;  // pending corrected values, one stage per tile
+  static constexpr int kXL = kGates ? kX : 0;       // low halves of [Q~; K~], same chunk layout
+  static constexpr int kG = kGates ? NP * DK * 4 : 0;      // the draft's per-key gates
+  static constexpr int kPg = kGates ? kPMax * DK * 4 : 0;  // pending per-key gates
   static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 4 + 16;
-  static constexpr int kBytes = kX + kT + kAt + kLk + kPk + kPu + kTopo;
+  static constexpr int oT = kX, oAt = oT + kT, oLk = oAt + kAt, oPk = oLk + kLk, oPu = oPk + kPk;
+  static constexpr int oXL = oPu + kPu, oG = oXL + kXL, oPg = oG + kG, oTopo = oPg + kPg;
+  static constexpr int kBytes = oTopo + kTopo;
 };
 
 // [Q; K] chunk (row, c) lives at row * CH + (c ^ (row & 7)): the 16 rows a
@@ -129,12 +145,14 @@ __device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x
 template <int DK, int NP, int TPW>
 constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
 
-// DELTA: the delta-rule families (GDN, DeltaNet).  Without the delta rule
-// (scalar decay) Lk = 0, so T = I and U = R = V: no P_k, no Lk, no T.
-template <int DK, int NP, int CW, int TPW, bool DELTA>
+// KIND: the family's form (see Layout).  Without the delta rule Lk = 0, so
+// T = I and U = R = V: no P_k, no Lk, no T.
+template <int DK, int NP, int CW, int TPW, int KIND>
 __global__ __launch_bounds__((CW + 1) * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
 void verify_tile_kernel(VerifyArgs a) {
-  using L = Layout<DK, NP, CW, TPW>;
+  using L = Layout<DK, NP, CW, TPW, KIND>;
+  constexpr bool DELTA = KIND == kKindDelta;
+  constexpr bool GV = KIND == kKindGates;
   constexpr int kColWaves = CW;                 // waves 0 .. CW-1 own state columns
   constexpr int kSetup = CW;                    // the setup wave
   constexpr int kTileCols = L::kTileCols;       // state columns per workgroup
@@ -143,13 +161,16 @@ void verify_tile_kernel(VerifyArgs a) {
   constexpr int GT = (NGT + kColWaves - 1) / kColWaves;     // Gram tiles per column wave
 
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  uint4 *xs = reinterpret_cast<uint4 *>(lds);                              // [Q; K]
-  float *tb = reinterpret_cast<float *>(lds + L::kX);                      // T blocks
-  float *ab = reinterpret_cast<float *>(lds + L::kX + L::kT);              // Attn blocks
-  float *lk = reinterpret_cast<float *>(lds + L::kX + L::kT + L::kAt);     // compact Lk
-  bf16 *s_pk = reinterpret_cast<bf16 *>(lds + L::kX + L::kT + L::kAt + L::kLk);             // [kPMax][DK]
-  float *s_pu = reinterpret_cast<float *>(lds + L::kX + L::kT + L::kAt + L::kLk + L::kPk);  // [kPMax][64]
-  unsigned char *tp = lds + L::kX + L::kT + L::kAt + L::kLk + L::kPk + L::kPu;
+  uint4 *xs = reinterpret_cast<uint4 *>(lds);                 // [Q; K] (GLA: high halves of [Q~; K~])
+  float *tb = reinterpret_cast<float *>(lds + L::oT);         // T blocks
+  float *ab = reinterpret_cast<float *>(lds + L::oAt);        // Attn blocks
+  float *lk = reinterpret_cast<float *>(lds + L::oLk);        // compact Lk
+  bf16 *s_pk = reinterpret_cast<bf16 *>(lds + L::oPk);        // [kPMax][DK]
+  float *s_pu = reinterpret_cast<float *>(lds + L::oPu);      // [kPMax][64]
+  uint4 *xl = reinterpret_cast<uint4 *>(lds + L::oXL);        // GLA: low halves of [Q~; K~]
+  float *s_g = reinterpret_cast<float *>(lds + L::oG);        // GLA: [NP][DK] gates
+  float *s_pg = reinterpret_cast<float *>(lds + L::oPg);      // GLA: [kPMax][DK] pending gates
+  unsigned char *tp = lds + L::oTopo;
   uint64_t *s_anc = reinterpret_cast<uint64_t *>(tp);      // [NP]
   int *s_depth = reinterpret_cast<int *>(tp + 8 * NP);     // [NP]
   int *s_off = s_depth + NP;                                // [NP]
@@ -228,7 +249,8 @@ void verify_tile_kernel(VerifyArgs a) {
     const bool live = l < n;
     const size_t s = (nbase + (live ? l : 0)) * H + h;
     p = live ? a.parent[nbase + l] : -1;
-    al = (live && a.family != SLA_FAMILY_DELTANET) ? a.alpha[s] : 1.f;  // DeltaNet: no decay
+    // DeltaNet: no decay; GLA: the per-key gates enter through Q~ and K~
+    al = (!GV && live && a.family != SLA_FAMILY_DELTANET) ? a.alpha[s] : 1.f;
     const float be = (DELTA && live) ? a.beta[s] : 0.f;
     // pending accepted path, with the previous round's parent row and gates
     // read whole, so that validating the path waits on no further read
@@ -240,7 +262,7 @@ void verify_tile_kernel(VerifyArgs a) {
       plen = a.pend.len[b];
       node = l < pn ? a.pend.path[prow + l] : -1;
       prow_parent = l < pn ? a.pend.parent[prow + l] : -2;
-      prow_alpha = l < pn ? a.pend.alpha[(prow + l) * H + h] : 0.f;
+      prow_alpha = (!GV && l < pn) ? a.pend.alpha[(prow + l) * H + h] : 0.f;
     }
     // [Q; K] straight into LDS (rows 0..NP-1: q_j, NP..2NP-1: k_j; padding
     // rows repeat node 0 and are never used)
@@ -250,6 +272,15 @@ void verify_tile_kernel(VerifyArgs a) {
       const int row = P / CH, c = (P % CH) ^ (row & 7);
       const int j = row % NP;
       load_lds16((row < NP ? qg : kg) + ((nbase + (j < n ? j : 0)) * H + h) * DK + c * 8, xs + i * kWave);
+    }
+    if constexpr (GV) {  // the draft's per-key gates, rows 0..NP-1 (padding rows repeat node 0)
+      constexpr int GC = DK / 4;  // 16-byte chunks per gate row
+#pragma unroll 1
+      for (int i = 0; i < NP * GC / kWave; ++i) {
+        const int P = i * kWave + l;
+        const int j = P / GC;
+        load_lds16(a.alpha + ((nbase + (j < n ? j : 0)) * H + h) * DK + (P % GC) * 4, s_g + i * kWave * 4);
+      }
     }
 
     // topology, decays and compact-list offsets; lane j owns node j
@@ -339,17 +370,89 @@ void verify_tile_kernel(VerifyArgs a) {
   if (w == kSetup && a.has_pending) {
     const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
     constexpr int KI = kPMax * CH / kWave;
-    int nt[KI];  // node of the step whose key chunk this lane gathers
+    constexpr int GC = DK / 4;                             // 16-byte chunks per gate row
+    constexpr int GI = GV ? kPMax * GC / kWave : 0;
+    int nt[KI], ng[GI > 0 ? GI : 1];  // node of the step whose key (gate) chunk this lane gathers
 #pragma unroll
     for (int i = 0; i < KI; ++i) nt[i] = __shfl(nodec, (i * kWave + l) / CH);
+#pragma unroll
+    for (int i = 0; i < GI; ++i) ng[i] = __shfl(nodec, (i * kWave + l) / GC);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < KI; ++i)
       load_lds16(pkg + ((prow + nt[i]) * H + h) * DK + ((i * kWave + l) % CH) * 8, s_pk + i * kWave * 8);
+#pragma unroll
+    for (int i = 0; i < GI; ++i)
+      load_lds16(a.pend.alpha + ((prow + ng[i]) * H + h) * DK + ((i * kWave + l) % GC) * 4, s_pg + i * kWave * 4);
     // every tile's values at once: a later tile's would otherwise be waited
     // for on the critical path
 #pragma unroll
     for (int i = 0; i < TPW; ++i) gather_u(t0 + i, i);
+  }
+
+  // ---- GLA: Gamma_j = product of the gates over P(j) per key dimension, then
+  //      Q~_j = Gamma_j * q_j and K~_j = k_j / Gamma_j split into bf16 hi (in
+  //      place of q_j, k_j) + lo; one lane per (node, 4 key dimensions).  The
+  //      records (the key as given, the gates) are written from here.
+  if constexpr (GV) {
+    if (w < kColWaves) {
+      constexpr int C4 = DK / 4;
+      unsigned char *xb = reinterpret_cast<unsigned char *>(xs);
+      unsigned char *xlb = reinterpret_cast<unsigned char *>(xl);
+      for (int it = w * kWave + l; it < NP * C4; it += kColWaves * kWave) {
+        const int j = it / C4, c4 = it % C4;
+        const int oq = xchunk<CH>(j, c4 >> 1) * 16 + (c4 & 1) * 8;
+        const int ok = xchunk<CH>(NP + j, c4 >> 1) * 16 + (c4 & 1) * 8;
+        if (j >= n) {  // padding rows: zero low halves (their products are masked or dropped)
+          *reinterpret_cast<uint2 *>(xlb + oq) = make_uint2(0, 0);
+          *reinterpret_cast<uint2 *>(xlb + ok) = make_uint2(0, 0);
+          continue;
+        }
+        float G[4] = {1.f, 1.f, 1.f, 1.f};
+        for (uint64_t m = s_anc[j]; m; m &= m - 1ull) {
+          const float4 gx = *reinterpret_cast<const float4 *>(s_g + __builtin_ctzll(m) * DK + 4 * c4);
+          G[0] *= gx.x;
+          G[1] *= gx.y;
+          G[2] *= gx.z;
+          G[3] *= gx.w;
+        }
+        const uint2 qb = *reinterpret_cast<const uint2 *>(xb + oq);
+        const uint2 kb = *reinterpret_cast<const uint2 *>(xb + ok);
+        const uint32_t qw[2] = {qb.x, qb.y}, kw[2] = {kb.x, kb.y};
+        uint32_t qh[2], ql[2], kh[2], kl[2];
+#pragma unroll
+        for (int e2 = 0; e2 < 2; ++e2) {
+          uint32_t hq = 0, lq = 0, hk = 0, lk2 = 0;
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int e = 2 * e2 + s2;
+            const float qf = __uint_as_float((s2 ? qw[e2] >> 16 : qw[e2] & 0xffffu) << 16) * G[e];
+            const float kf = __uint_as_float((s2 ? kw[e2] >> 16 : kw[e2] & 0xffffu) << 16) / G[e];
+            const __bf16 qhi = static_cast<__bf16>(qf), khi = static_cast<__bf16>(kf);
+            const __bf16 qlo = static_cast<__bf16>(qf - static_cast<float>(qhi));
+            const __bf16 klo = static_cast<__bf16>(kf - static_cast<float>(khi));
+            hq |= (uint32_t)__builtin_bit_cast(uint16_t, qhi) << (16 * s2);
+            lq |= (uint32_t)__builtin_bit_cast(uint16_t, qlo) << (16 * s2);
+            hk |= (uint32_t)__builtin_bit_cast(uint16_t, khi) << (16 * s2);
+            lk2 |= (uint32_t)__builtin_bit_cast(uint16_t, klo) << (16 * s2);
+          }
+          qh[e2] = hq;
+          ql[e2] = lq;
+          kh[e2] = hk;
+          kl[e2] = lk2;
+        }
+        *reinterpret_cast<uint2 *>(xb + oq) = make_uint2(qh[0], qh[1]);
+        *reinterpret_cast<uint2 *>(xlb + oq) = make_uint2(ql[0], ql[1]);
+        *reinterpret_cast<uint2 *>(xb + ok) = make_uint2(kh[0], kh[1]);
+        *reinterpret_cast<uint2 *>(xlb + ok) = make_uint2(kl[0], kl[1]);
+        if (t0 == 0) {
+          const size_t r = ((nbase + j) * H + h) * DK + 4 * c4;
+          *reinterpret_cast<uint2 *>(static_cast<bf16 *>(a.fk) + r) = kb;
+          *reinterpret_cast<float4 *>(a.falpha + r) = *reinterpret_cast<const float4 *>(s_g + j * DK + 4 * c4);
+        }
+      }
+    }
+    __syncthreads();
   }
 
   // ---- tree-masked Grams over the column waves: tile (mr, na) of [Q; K] K^T holds
@@ -369,6 +472,12 @@ void verify_tile_kernel(VerifyArgs a) {
           const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mr * 16 + lc, ks * 4 + lg));
           const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
           g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, g, 0, 0, 0);
+          if constexpr (GV) {  // Q~ K~^T = hi hi + hi lo + lo hi
+            const bf16x8 al8 = *reinterpret_cast<const bf16x8 *>(xl + xchunk<CH>(mr * 16 + lc, ks * 4 + lg));
+            const bf16x8 bl8 = *reinterpret_cast<const bf16x8 *>(xl + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
+            g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bl8, g, 0, 0, 0);
+            g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al8, bf, g, 0, 0, 0);
+          }
         }
         gacc[tc / kColWaves] = g;
       }
@@ -507,27 +616,38 @@ void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
           for (int k0 = 0; k0 < KS; k0 += KC) {
             bf16x8 kv[KC];
+            float gv[KC][8];  // GLA: the gates of rows 32 (k0 + c) + 8 lg + e
 #pragma unroll
             for (int c = 0; c < KC; ++c) kv[c] = *reinterpret_cast<const bf16x8 *>(s_pk + st * DK + (k0 + c) * 32 + 8 * lg);
+            if constexpr (GV) {
+#pragma unroll
+              for (int c = 0; c < KC; ++c) {
+                const float4 g0 = *reinterpret_cast<const float4 *>(s_pg + st * DK + (k0 + c) * 32 + 8 * lg);
+                const float4 g1 = *reinterpret_cast<const float4 *>(s_pg + st * DK + (k0 + c) * 32 + 8 * lg + 4);
+                gv[c][0] = g0.x, gv[c][1] = g0.y, gv[c][2] = g0.z, gv[c][3] = g0.w;
+                gv[c][4] = g1.x, gv[c][5] = g1.y, gv[c][6] = g1.z, gv[c][7] = g1.w;
+              }
+            }
 #pragma unroll
             for (int c = 0; c < KC; ++c)
 #pragma unroll
               for (int e = 0; e < 8; ++e)
-                hf[k0 + c][e] = apply_factor(hf[k0 + c][e], al, static_cast<float>(kv[c][e]), uv);
+                hf[k0 + c][e] = apply_factor(hf[k0 + c][e], GV ? gv[c][e] : al, static_cast<float>(kv[c][e]), uv);
           }
         }
         // paths longer than the LDS stage read their records directly
         for (int st = kPMax; st < plen; ++st) {
           const int node = a.pend.path[(size_t)b * pn + st];
           const size_t r = ((size_t)b * pn + node) * H + h;
-          const float al = a.pend.alpha[r];
+          const float al = GV ? 1.f : a.pend.alpha[r];
           const float uv = a.pend.u[r * dv + col];
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks) {
-            float kr[8];
+            float kr[8], gr[8];
             load_f32<8>(pkg + r * DK + ks * 32 + 8 * lg, kr);
+            if constexpr (GV) load_f32<8>(a.pend.alpha + r * DK + ks * 32 + 8 * lg, gr);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], al, kr[e], uv);
+            for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], GV ? gr[e] : al, kr[e], uv);
           }
         }
         // committed rows back with the default policy: a wave writes half of
@@ -581,6 +701,10 @@ void verify_tile_kernel(VerifyArgs a) {
           const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
           pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pq[mt], 0, 0, 0);
           pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pq[mt], 0, 0, 0);
+          if constexpr (GV) {  // Q~ lo half
+            const bf16x8 afl = *reinterpret_cast<const bf16x8 *>(xl + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
+            pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afl, bhi, pq[mt], 0, 0, 0);
+          }
         }
       }
     }
@@ -596,13 +720,15 @@ void verify_tile_kernel(VerifyArgs a) {
     // alpha, parent -- while the column waves compute the first tile's
     // products (off the path to the barrier above)
     if (w == kSetup && i == 0 && t0 == 0) {
-      bf16 *fk = static_cast<bf16 *>(a.fk);
-      for (int c = l; c < n * CH; c += kWave) {
-        const int j = c / CH, part = c % CH;
-        *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * 8) = xs[xchunk<CH>(NP + j, part)];
+      if constexpr (!GV) {  // GLA's key and gate records went out with Q~, K~
+        bf16 *fk = static_cast<bf16 *>(a.fk);
+        for (int c = l; c < n * CH; c += kWave) {
+          const int j = c / CH, part = c % CH;
+          *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * 8) = xs[xchunk<CH>(NP + j, part)];
+        }
       }
       if (l < n) {
-        a.falpha[(nbase + l) * H + h] = al;
+        if constexpr (!GV) a.falpha[(nbase + l) * H + h] = al;
         if (h == 0) a.fparent[nbase + l] = p;
       }
     }
@@ -684,12 +810,12 @@ int device_cus() {
 // hold them back briefly instead (stagger).
 constexpr int kLateRounds = 4;
 
-template <int DK, int NP, int CW, int TPW, bool DELTA>
+template <int DK, int NP, int CW, int TPW, int KIND>
 hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
-  using L = Layout<DK, NP, CW, TPW>;
+  using L = Layout<DK, NP, CW, TPW, KIND>;
   const size_t lds = L::kBytes;
   if (lds > kMaxLds) return hipErrorInvalidConfiguration;
-  auto kern = verify_tile_kernel<DK, NP, CW, TPW, DELTA>;
+  auto kern = verify_tile_kernel<DK, NP, CW, TPW, KIND>;
   if (lds > kDefaultLds) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -713,8 +839,9 @@ hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
 
 template <int DK, int NP, int CW, int TPW>
 hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
-  if (a.family == SLA_FAMILY_DECAY) return launch_np_fam<DK, NP, CW, TPW, false>(a, s);
-  return launch_np_fam<DK, NP, CW, TPW, true>(a, s);
+  if (a.family == SLA_FAMILY_GLA) return launch_np_fam<DK, NP, CW, TPW, kKindGates>(a, s);
+  if (a.family == SLA_FAMILY_DECAY) return launch_np_fam<DK, NP, CW, TPW, kKindDecay>(a, s);
+  return launch_np_fam<DK, NP, CW, TPW, kKindDelta>(a, s);
 }
 
 template <int DK>

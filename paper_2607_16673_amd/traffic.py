@@ -106,7 +106,7 @@ def _per_dispatch_kib(rows, tag, skip=0):
 
 
 def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, json_path: str,
-              kernel: str = KERNEL_TAG) -> dict:
+              kernel: str = KERNEL_TAG, family: str = "gdn") -> dict:
     copy_bytes = COPY_MIB * (1 << 20)  # per copy dispatch, read and written
     cf, _ = _per_dispatch_kib(_rows(os.path.join(out_dir, "copy_fetch"), "FETCH_SIZE"), COPY_TAG, 0)
     cw, _ = _per_dispatch_kib(_rows(os.path.join(out_dir, "copy_write"), "WRITE_SIZE"), COPY_TAG, 0)
@@ -117,6 +117,8 @@ def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, jso
     fetch = bf * 1024.0 * scale_f
     write = bw * 1024.0 * scale_w
     key = "%s/%s/%s" % (workload, route, mode)
+    if family != "gdn":
+        key += "/" + family
     entry = {
         "kernel": kernel,
         "bytes_per_launch": int(round(fetch + write)),
@@ -200,6 +202,7 @@ def main(argv=None) -> None:
     s.add_argument("--route", default="auto", help="auto, serial, parallel, or conv for the convolution")
     s.add_argument("--kernel", default=KERNEL_TAG, help="kernel name substring to average")
     s.add_argument("--mode", default="fused")
+    s.add_argument("--family", default="gdn", help="layer family the bench ran (bench.py --family)")
     s.add_argument("--skip", type=int, default=0,
                    help="leading verify dispatches to ignore (the first step has no pending path)")
     s.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
@@ -214,7 +217,8 @@ def main(argv=None) -> None:
     elif a.cmd == "mfma":
         print(json.dumps(summarize_mfma(a.out_dir, a.workload, a.skip, a.json), indent=1))
     else:
-        print(json.dumps(summarize(a.out_dir, a.workload, a.route, a.mode, a.skip, a.json, a.kernel), indent=1))
+        print(json.dumps(summarize(a.out_dir, a.workload, a.route, a.mode, a.skip, a.json, a.kernel, a.family),
+                         indent=1))
 
 
 if __name__ == "__main__":

@@ -1,6 +1,6 @@
 """GPU parity of the other layer families (DeltaNet, scalar decay without the
 delta rule, GLA's per-key gates; the factor-record remark closing §5.1)
-against the fp64 oracle, through the C ABI.
+against the fp64 oracle, through the C ABI, on both verification routes.
 
 Per case: round 0 verified from the committed state (outputs against the
 oracle, factor records against their definition: the key and gate copies
@@ -109,8 +109,10 @@ CASES = [(name, fam, route)
                       "batched_tree_serving", "large_batch_tree64"]
          for fam in ["deltanet", "decay", "gla"]
          for route in ["serial", "parallel"]
-         if not (route == "parallel" and (fam == "gla" or name == "tiny_chain_f32"))]
-CASES.append((GLA_DK256_N50.name, "gla", "serial"))
+         if not (route == "parallel" and name == "tiny_chain_f32")]
+# the largest GLA draft at d_k = 256 exceeds the parallel route's on-chip stage:
+# the automatic route falls back to the serial one
+CASES += [(GLA_DK256_N50.name, "gla", "serial"), (GLA_DK256_N50.name, "gla", "auto")]
 
 
 @pytest.mark.parametrize("name,fam,route", CASES)
@@ -174,6 +176,16 @@ def test_family_two_rounds(name, fam, route):
     err1 = rel_err(np.stack([got[b, :, h] for b, h in units]), _oracle_out(refS, d1, units, fam))
     say("  round 1 output rel err %.3e" % err1)
     assert err1 <= tol
+
+
+def test_gla_parallel_route_refuses_drafts_beyond_its_stage():
+    cfg = GLA_DK256_N50
+    d = Draft(cfg, "gla", 0)
+    state = torch.from_numpy(inputs.draw_state(cfg, 0)).cuda()
+    out = torch.empty(cfg.batch, cfg.n_nodes, cfg.heads, cfg.d_v, device="cuda")
+    with pytest.raises(B.SlaError) as e:
+        _verify(cfg, "gla", "parallel", state, d, out, _factors(cfg, "gla"))
+    assert e.value.code == B.SLA_ERR_UNSUPPORTED
 
 
 def test_gla_draft_beyond_the_on_chip_stage_is_rejected():
