@@ -60,14 +60,16 @@ constexpr int kBP = 20;                           // fp32 row pitch of a 16x16 b
 constexpr int kZ = 8;                             // root paths up to this depth solve T in registers
 
 // Layer families by the form of their step (template parameter KIND):
-//   kKindDelta  GDN and DeltaNet: the delta rule, scalar gate;
-//   kKindDecay  scalar decay without the delta rule: Lk = 0, T = I, U = V;
+//   kKindDelta  scalar gates: GDN, DeltaNet (alpha = 1) and the scalar decay
+//               without the delta rule (beta = 0, so Lk = 0 and T = I, with
+//               R = V in place of beta (v - gamma P_k): a run-time choice,
+//               so that all three share one register allocation);
 //   kKindGates  GLA: one gate per key dimension, no delta rule.  The decay
 //               ratios become per-dimension, D_ja[i] = Gamma_j[i] / Gamma_a[i],
 //               and fold into the operands: Q~_j = Gamma_j * q_j and
 //               K~_a = k_a / Gamma_a (fp32, split into bf16 hi + lo), so
 //               Attn_ja = Q~_j . K~_a and O = Q~ H0 + Attn V.
-constexpr int kKindDelta = 0, kKindDecay = 1, kKindGates = 2;
+constexpr int kKindDelta = 0, kKindGates = 1;
 
 template <int DK, int NP, int CW, int TPW, int KIND>
 struct Layout {
@@ -153,6 +155,7 @@ void verify_tile_kernel(VerifyArgs a) {
   using L = Layout<DK, NP, CW, TPW, KIND>;
   constexpr bool DELTA = KIND == kKindDelta;
   constexpr bool GV = KIND == kKindGates;
+  const bool nodelta = !DELTA || a.family == SLA_FAMILY_DECAY;  // R = V
   constexpr int kColWaves = CW;                 // waves 0 .. CW-1 own state columns
   constexpr int kSetup = CW;                    // the setup wave
   constexpr int kTileCols = L::kTileCols;       // state columns per workgroup
@@ -251,7 +254,7 @@ void verify_tile_kernel(VerifyArgs a) {
     p = live ? a.parent[nbase + l] : -1;
     // DeltaNet: no decay; GLA: the per-key gates enter through Q~ and K~
     al = (!GV && live && a.family != SLA_FAMILY_DELTANET) ? a.alpha[s] : 1.f;
-    const float be = (DELTA && live) ? a.beta[s] : 0.f;
+    const float be = (DELTA && live && a.family != SLA_FAMILY_DECAY) ? a.beta[s] : 0.f;
     // pending accepted path, with the previous round's parent row and gates
     // read whole, so that validating the path waits on no further read
     int plen = 0, node = -1, prow_parent = -2;
@@ -690,7 +693,8 @@ void verify_tile_kernel(VerifyArgs a) {
           uint32_t vb = vraw[mt][q];
           __asm__("" : "+v"(vb));  // keeps the widening here, not next to the load
           const float vf = __uint_as_float(vb << 16);
-          rreg[mt][q] = j < n ? (DELTA ? s_be[j] * (vf - s_gamma[j] * pk[mt][q]) : vf) : 0.f;
+          const float rd = DELTA ? s_be[j] * (vf - s_gamma[j] * pk[mt][q]) : vf;
+          rreg[mt][q] = j < n ? (nodelta ? vf : rd) : 0.f;
         }
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
@@ -840,7 +844,6 @@ hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
 template <int DK, int NP, int CW, int TPW>
 hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
   if (a.family == SLA_FAMILY_GLA) return launch_np_fam<DK, NP, CW, TPW, kKindGates>(a, s);
-  if (a.family == SLA_FAMILY_DECAY) return launch_np_fam<DK, NP, CW, TPW, kKindDecay>(a, s);
   return launch_np_fam<DK, NP, CW, TPW, kKindDelta>(a, s);
 }
 
