@@ -201,3 +201,88 @@ def test_gla_draft_beyond_the_on_chip_stage_is_rejected():
         B.sla_verify(z(1, 1, 256, 16, device="cuda"), q, q, v, z(1, n, 1, 256, device="cuda"), None, par,
                      z(1, n, 1, 16, device="cuda"), f, family="gla")
     assert e.value.code == B.SLA_ERR_UNSUPPORTED
+
+
+# ------------------------------------------------------------ random shapes
+def _sweep_cases(seed, count):
+    r = np.random.default_rng(seed)
+    out = []
+    for i in range(count):
+        out.append((i, ["deltanet", "decay", "gla"][i % 3], int(r.integers(1, 5)), int(r.integers(1, 4)),
+                    int(r.choice([64, 128, 256])), int(r.choice([16, 48, 64, 80, 128, 144, 192])),
+                    int(r.choice([1, 3, 16, 17, 32, 33, 50, 64])), int(r.choice([1, 2, 15, 31, 40, 64])),
+                    int(r.integers(0, 1 << 30))))
+    return out
+
+
+SWEEP = _sweep_cases(11, 18)
+
+
+def _random_parent(r, Bn, n):
+    rows = []
+    for b in range(Bn):
+        if b % 2:
+            rows.append(np.array([int(r.integers(-1, j)) if j else -1 for j in range(n)], np.int32))
+        else:
+            rows.append(inputs.random_tree(r, n, max(2, n // 2), 4))
+    return np.stack(rows)
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=["s%d_%s_B%d_H%d_dk%d_dv%d_n%d-%d" % c[:8] for c in SWEEP])
+@pytest.mark.parametrize("route", ["auto", "serial"])
+def test_family_sweep_two_fused_rounds(case, route):
+    """Random shapes (d_k 64/128/256, ragged d_v, node counts across the
+    16/32/64 blocks, trees and forests, pending rounds of another size):
+    two fused rounds against verify + standalone commit bitwise, and the
+    committed state and second outputs against the oracle."""
+    i, fam, Bn, H, dk, dv, n0, n1, seed = case
+    r = np.random.default_rng(seed)
+    say("family sweep %d %s route %s: B=%d H=%d dk=%d dv=%d n0=%d n1=%d" % (i, fam, route, Bn, H, dk, dv, n0, n1))
+    cfgs = [inputs.Config("fs%d" % k, 700 + 2 * i + k, Bn, H, dk, dv, n, False, n, 64, inputs.BF16, 1)
+            for k, n in ((0, n0), (1, n1))]
+    drafts = []
+    for k, cfg in enumerate(cfgs):
+        d = Draft(cfg, fam, 0)
+        d.rnd.parent = _random_parent(r, Bn, cfg.n_nodes)
+        d.parent = _dev(d.rnd.parent)
+        drafts.append(d)
+    d0, d1 = drafts
+    path = np.full((Bn, n0), -1, np.int32)
+    ln = np.zeros(Bn, np.int32)
+    for b in range(Bn):
+        if r.random() < 0.85:
+            p = inputs.walk_to_root(d0.rnd.parent[b], int(r.integers(0, n0)))
+            path[b, :len(p)] = p
+            ln[b] = len(p)
+    d0.rnd.path, d0.rnd.length = path, ln
+    d0.path, d0.length = _dev(path), _dev(ln)
+    S0 = inputs.draw_state(cfgs[0], 0)
+    too_big = fam == "gla" and dk == 256 and max(n0, n1) > 50
+    f0, f1, g0, g1 = (_factors(c, fam) for c in (cfgs[0], cfgs[1], cfgs[0], cfgs[1]))
+    out1, o1 = (torch.empty(Bn, n1, H, dv, device="cuda") for _ in range(2))
+    fused = torch.from_numpy(S0).cuda()
+    if too_big:
+        with pytest.raises(B.SlaError) as e:
+            _verify(cfgs[0] if n0 > 50 else cfgs[1], fam, route, fused, d0 if n0 > 50 else d1,
+                    torch.empty(Bn, max(n0, n1), H, dv, device="cuda"), f0 if n0 > 50 else f1)
+        assert e.value.code == B.SLA_ERR_UNSUPPORTED
+        return
+    _verify(cfgs[0], fam, route, fused, d0, torch.empty(Bn, n0, H, dv, device="cuda"), f0)
+    st = _verify(cfgs[1], fam, route, fused, d1, out1, f1, pending=(f0, d0.path, d0.length))
+    sep = torch.from_numpy(S0).cuda()
+    _verify(cfgs[0], fam, route, sep, d0, torch.empty(Bn, n0, H, dv, device="cuda"), g0)
+    B.sla_commit(sep, g0, d0.path, d0.length, family=fam)
+    _verify(cfgs[1], fam, route, sep, d1, o1, g1)
+    torch.cuda.synchronize()
+    assert (st.cpu().numpy() == 0).all()
+    assert torch.equal(fused, sep)
+    assert torch.equal(out1, o1)
+    units = [(b, h) for b in range(Bn) for h in range(H)]
+    if len(units) > 6:
+        units = [units[j] for j in sorted(r.choice(len(units), 6, replace=False))]
+    refS = _oracle_commit(S0, d0, units, fam)
+    es = rel_err(np.stack([fused.cpu().numpy()[b, h] for b, h in units]), np.stack([refS[u] for u in units]))
+    got = out1.cpu().numpy()
+    eo = rel_err(np.stack([got[b, :, h] for b, h in units]), _oracle_out(refS, d1, units, fam))
+    say("  state err %.2e output err %.2e" % (es, eo))
+    assert es <= TOL[inputs.BF16] and eo <= TOL[inputs.BF16]
