@@ -61,6 +61,7 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 constexpr int kBufWord3 = 0x00020000;  // raw 32-bit dword access, no swizzle
 constexpr int kPolicyDefault = 0;
 constexpr int kPolicyStream = 2;  // non-temporal: data touched once
+constexpr int kPolicyStreamDevice = 18;  // non-temporal, written through at device scope (nt | sc1)
 
 __device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes, kBufWord3);

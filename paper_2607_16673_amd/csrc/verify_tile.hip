@@ -148,8 +148,9 @@ template <int DK, int NP, int TPW>
 constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
 
 // KIND: the family's form (see Layout).  Without the delta rule Lk = 0, so
-// T = I and U = R = V: no P_k, no Lk, no T.
-template <int DK, int NP, int CW, int TPW, int KIND>
+// T = I and U = R = V: no P_k, no Lk, no T.  WT: committed rows written
+// through at device scope (launches of one round of workgroups).
+template <int DK, int NP, int CW, int TPW, int KIND, bool WT>
 __global__ __launch_bounds__((CW + 1) * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
 void verify_tile_kernel(VerifyArgs a) {
   using L = Layout<DK, NP, CW, TPW, KIND>;
@@ -653,14 +654,22 @@ void verify_tile_kernel(VerifyArgs a) {
             for (int e = 0; e < 8; ++e) hf[ks][e] = apply_factor(hf[ks][e], GV ? gr[e] : al, kr[e], uv);
           }
         }
-        // committed rows back with the default policy: a wave writes half of
-        // each 128-byte line and the neighbouring wave the other half, and
-        // with a streaming hint the halves leave the L2 separately (measured:
-        // 8% more HBM writes and 4.7% longer launches)
+        // committed rows back.  A wave writes half of each 128-byte line and
+        // the neighbouring wave the other half.  Over many rounds of
+        // workgroups the default policy lets the L2 merge the halves (a plain
+        // streaming hint wrote them separately: 8% more HBM writes, 4.7%
+        // longer launches).  In a single round the rows are written through
+        // at device scope instead: what stays dirty in the L2 is written back
+        // at the end of the kernel, on its critical path (measured at batched
+        // tree serving 39.2 -> 37.9 us per launch; on the 1-node decode chain,
+        // eight rounds, the default policy stays 2% faster).
+        // (chosen at launch: a run-time branch between the two store loops
+        // cost most of the gain)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) buf_store_f32<kPolicyDefault>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
+          for (int e = 0; e < 8; ++e)
+            buf_store_f32<WT ? kPolicyStreamDevice : kPolicyDefault>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
       }
       // P_k = K H0 first (hi/lo split, K-step by K-step as the tile lands),
       // so that R = beta (v - gamma P_k) takes its place before P_q is built:
@@ -819,11 +828,14 @@ hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
   using L = Layout<DK, NP, CW, TPW, KIND>;
   const size_t lds = L::kBytes;
   if (lds > kMaxLds) return hipErrorInvalidConfiguration;
-  auto kern = verify_tile_kernel<DK, NP, CW, TPW, KIND>;
+  auto kern_wb = verify_tile_kernel<DK, NP, CW, TPW, KIND, false>;  // committed rows written back
+  auto kern_wt = verify_tile_kernel<DK, NP, CW, TPW, KIND, true>;   // written through
   if (lds > kDefaultLds) {
-    const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-    if (e != hipSuccess) return e;
+    for (auto k : {kern_wb, kern_wt}) {
+      const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+    }
   }
   const int ntiles = (a.dv + L::kTileCols - 1) / L::kTileCols;
   const size_t groups = (size_t)a.B * a.H * ((ntiles + TPW - 1) / TPW);
@@ -831,13 +843,13 @@ hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
   // resident workgroups per CU for this instantiation (registers, LDS, waves)
   static const int per_cu = [&] {
     int k = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&k, kern, (CW + 1) * kWave, lds) != hipSuccess || k < 1) k = 1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&k, kern_wb, (CW + 1) * kWave, lds) != hipSuccess || k < 1) k = 1;
     return k;
   }();
   const size_t slots = (size_t)per_cu * device_cus();
   b.late_state = groups >= (size_t)kLateRounds * slots;
   b.stagger = !b.late_state && groups >= slots;
-  hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3((CW + 1) * kWave), lds, s, b);
+  hipLaunchKernelGGL(b.late_state ? kern_wb : kern_wt, dim3((unsigned)groups), dim3((CW + 1) * kWave), lds, s, b);
   return hipGetLastError();
 }
 
