@@ -13,6 +13,8 @@
 namespace sla {
 namespace {
 
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+
 constexpr int kCommitThreads = 256;
 constexpr int kCommitCols = 64;   // state columns per workgroup
 constexpr int kCommitStage = 8;   // path records staged in LDS; longer paths read the rest directly
@@ -135,8 +137,21 @@ __global__ __launch_bounds__(kCommitThreads) void commit_kernel(CommitArgs a) {
     }
   }
   if (len == 0) return;
+  // whole lines; with a workgroup per CU or more, written through at device
+  // scope, so that nothing is left dirty in the L2 for the end of the kernel
+  // (measured against plain stores: the separate route at batched tree
+  // serving 55.3 -> 48.4 us per layer, the 1-node decode chain 334 -> 293 us)
+  if (a.write_through) {
+    const rsrc_t sr = make_rsrc(st, (uint32_t)DK * dv * 4);
 #pragma unroll
-  for (int r = 0; r < R; ++r) *reinterpret_cast<float4 *>(st + (size_t)(tid / 16 + 16 * r) * dv + cg) = x[r];
+    for (int r = 0; r < R; ++r) {
+      const u32x4 v = {__float_as_uint(x[r].x), __float_as_uint(x[r].y), __float_as_uint(x[r].z), __float_as_uint(x[r].w)};
+      __builtin_amdgcn_raw_buffer_store_b128(v, sr, (uint32_t)(((tid / 16 + 16 * r) * dv + cg) * 4), 0, kPolicyStreamDevice);
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) *reinterpret_cast<float4 *>(st + (size_t)(tid / 16 + 16 * r) * dv + cg) = x[r];
+  }
 }
 
 __global__ __launch_bounds__(kWave) void topology_kernel(TopologyArgs a) {
@@ -154,11 +169,21 @@ __global__ __launch_bounds__(kWave) void topology_kernel(TopologyArgs a) {
   a.n_children[r + lane] = t.n_children;
 }
 
+int device_cus() {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    return 256;
+  return cus;
+}
+
 template <typename T, int DK>
 hipError_t launch_commit_dk(const CommitArgs &a, hipStream_t s) {
   auto kern = a.gate_vec ? commit_kernel<T, DK, true> : commit_kernel<T, DK, false>;
-  const dim3 grid((unsigned)((size_t)a.B * a.H * ((a.dv + kCommitCols - 1) / kCommitCols)));
-  hipLaunchKernelGGL(kern, grid, dim3(kCommitThreads), 0, s, a);
+  const size_t groups = (size_t)a.B * a.H * ((a.dv + kCommitCols - 1) / kCommitCols);
+  CommitArgs b = a;
+  b.write_through = groups >= (size_t)device_cus();
+  hipLaunchKernelGGL(kern, dim3((unsigned)groups), dim3(kCommitThreads), 0, s, b);
   return hipGetLastError();
 }
 

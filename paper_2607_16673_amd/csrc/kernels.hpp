@@ -40,7 +40,8 @@ struct VerifyArgs {
 
 struct CommitArgs {
   int32_t B, H, dk, dv, n;
-  bool gate_vec;  // alpha holds dk gates per record (GLA) instead of one
+  bool gate_vec;       // alpha holds dk gates per record (GLA) instead of one
+  bool write_through;  // state rows written through at device scope (at least one workgroup per CU)
   float *state;
   const void *k;
   const float *u;
