@@ -257,3 +257,47 @@ def test_full_size_fused_rounds(name, checked):
         ref, _ = oracle.conv_verify(Cref[bs], x32[bs], w, None, d.parent_np[bs])
         err = check_outputs(to_np(y)[bs], ref, cfg.dtype)
         say("conv full size %s: %d sequences, max elementwise rel err %.3e" % (name, len(bs), err))
+
+
+@pytest.mark.parametrize("dtype", [inputs.BF16, inputs.F32])
+@pytest.mark.parametrize("K", [1, 2, 3, 4])
+def test_one_node_drafts_fused_rounds(dtype, K):
+    """1-node drafts (the decode step, its own single-wave kernel): two rounds,
+    the first accepted or not per sequence, a ragged channel count and a bias;
+    the committed conv state bit-exact, outputs within the bars; a draft whose
+    only node names itself as parent is refused and leaves its state alone."""
+    r = np.random.default_rng(170 + K)
+    Bn, D = 5, 8 * 77
+    say("conv 1-node: %s K=%d" % (dtype, K))
+    d0 = random_draft(r, Bn, 1, D, dtype, kind="chain")
+    d1 = random_draft(r, Bn, 1, D, dtype, kind="chain")
+    d0.length_np[:] = [1, 0, 1, 1, 0]
+    d0.path_np[:, 0] = [0 if a else -1 for a in d0.length_np]
+    d0.length = torch.from_numpy(d0.length_np.copy()).cuda()
+    d0.path = torch.from_numpy(d0.path_np.copy()).cuda()
+    w = r.uniform(-0.5, 0.5, (D, K)).astype(np.float32)
+    bias = r.standard_normal(D).astype(np.float32)
+    C = inputs._to_dtype(r.standard_normal((Bn, K - 1, D)), inputs.BF16)[1].astype(np.float32)
+    Cg = torch.from_numpy(C).cuda() if K > 1 else None
+    wg, bg = torch.from_numpy(w).cuda(), torch.from_numpy(bias).cuda()
+    y0 = run_verify(Cg, d0, wg, bg, True)
+    st = torch.full((Bn,), 99, dtype=torch.int32, device="cuda")
+    y1 = run_verify(Cg, d1, wg, bg, True, pending=(d0.x, d0.parent, d0.path, d0.length), status=st)
+    torch.cuda.synchronize()
+    assert (st.cpu().numpy() == 0).all()
+    C0 = C if K > 1 else np.zeros((Bn, 0, D))
+    refC, _ = oracle.conv_commit(C0, d0.x32, d0.parent_np, d0.path_np, d0.length_np)
+    if K > 1:
+        np.testing.assert_array_equal(Cg.cpu().numpy().astype(np.float64), refC)
+    for y, d, Cref in [(y0, d0, C0), (y1, d1, refC)]:
+        ref, _ = oracle.conv_verify(Cref, d.x32, w, bias, d.parent_np)
+        check_outputs(to_np(y), ref, dtype)
+    bad = torch.zeros((Bn, 1), dtype=torch.int32, device="cuda")  # node 0 names itself
+    st2 = torch.full((Bn,), 99, dtype=torch.int32, device="cuda")
+    before = Cg.clone() if K > 1 else None
+    y2 = torch.empty_like(d1.x)
+    B.sla_conv_verify(Cg, d1.x, wg, bad, y2, bias=bg, pending=(d0.x, d0.parent, d0.path, d0.length), status=st2)
+    torch.cuda.synchronize()
+    assert (st2.cpu().numpy() == B.SLA_ERR_TOPOLOGY).all()
+    if K > 1:
+        assert torch.equal(Cg, before)
