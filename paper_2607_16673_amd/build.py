@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "libsla.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-SOURCES = ["api.cpp", "commit.hip", "conv.hip", "draft.hip", "verify_serial.hip", "verify_tile.hip"]
+SOURCES = ["api.cpp", "commit.hip", "conv.hip", "decode.hip", "draft.hip", "verify_serial.hip", "verify_tile.hip"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH, "-I" + INCLUDE, "-I" + CSRC,
           "-Wall", "-Wno-unused-result",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

@@ -188,8 +188,12 @@ int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pe
   a.falpha = factors->alpha;
   a.fparent = factors->parent;
   a.status = status;
-  hipError_t e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)
-                              : sla::launch_verify_serial(a, shape->qkv_dtype, stream);
+  hipError_t e;
+  if (route == SLA_ROUTE_AUTO && shape->n_nodes == 1)  // the decode step: its own streaming kernel
+    e = sla::launch_verify_decode(a, shape->qkv_dtype, stream);
+  else
+    e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)
+                     : sla::launch_verify_serial(a, shape->qkv_dtype, stream);
   // a draft whose on-chip stage does not fit the contraction's LDS (GLA's
   // per-key gates at the largest shapes) is refused before any launch; the
   // automatic route then takes the serial one

@@ -25,6 +25,7 @@ struct VerifyArgs {
   bool has_pending;
   bool late_state;  // parallel route: issue the state reads after the first barrier
   bool stagger;     // parallel route: hold the state reads back briefly (a full round of workgroups)
+  bool write_through;  // 1-node kernel: committed rows written through at device scope
   float *state;
   PendingArgs pend;
   const void *q, *k, *v;
@@ -67,6 +68,8 @@ struct TopologyArgs {
 hipError_t launch_verify_serial(const VerifyArgs &a, int dtype, hipStream_t s);
 bool parallel_supported(int dk, int dv, int n, int dtype);
 hipError_t launch_verify_parallel(const VerifyArgs &a, int dtype, hipStream_t s);
+// 1-node drafts (a.n == 1), any family and activation dtype
+hipError_t launch_verify_decode(const VerifyArgs &a, int dtype, hipStream_t s);
 hipError_t launch_commit(const CommitArgs &a, int dtype, hipStream_t s);
 hipError_t launch_topology(const TopologyArgs &a, hipStream_t s);
 

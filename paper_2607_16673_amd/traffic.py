@@ -41,7 +41,7 @@ COPY_TAG = "mul"  # the elementwise multiply of run_copy (not the fill before it
 # the sources each counted kernel is built from: counters taken on other
 # sources are stale
 SOURCES = {
-    "gdn": ["verify_tile.hip", "verify_serial.hip", "commit.hip", "device.hpp", "kernels.hpp"],
+    "gdn": ["verify_tile.hip", "verify_serial.hip", "decode.hip", "commit.hip", "device.hpp", "kernels.hpp"],
     "conv": ["conv.hip", "device.hpp", "layer_ops.hpp"],
 }
 
