@@ -72,7 +72,7 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   if (err != SLA_OK) return;
 
   // Stage this unit's draft in LDS.
-  extern __shared__ float lds[];
+  extern __shared__ __attribute__((aligned(16))) float lds[];
   float *ks = lds;                   // [n][DK]
   float *qs = ks + n * DK;           // [n][DK]
   float *gs = qs + n * DK;           // [n][DK] per-key gates (VG only)
@@ -88,12 +88,26 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   const T *q = static_cast<const T *>(a.q);
   const T *k = static_cast<const T *>(a.k);
   const T *v = static_cast<const T *>(a.v);
-  for (int idx = lane; idx < n * DK; idx += kWave) {
-    const int j = idx / DK, i = idx % DK;
+  // eight elements per lane and step (one 16-byte load of bf16, two of fp32)
+  for (int idx = lane; idx < n * (DK / 8); idx += kWave) {
+    const int j = idx / (DK / 8), i = (idx % (DK / 8)) * 8;
     const size_t src = (((size_t)b * n + j) * H + h) * DK + i;
-    ks[idx] = to_f32(k[src]);
-    qs[idx] = to_f32(q[src]);
-    if (VG) gs[idx] = a.alpha[src];
+    float kv[8], qv[8];
+    load_f32<8>(k + src, kv);
+    load_f32<8>(q + src, qv);
+    float4 *kd = reinterpret_cast<float4 *>(ks + j * DK + i);
+    float4 *qd = reinterpret_cast<float4 *>(qs + j * DK + i);
+    kd[0] = make_float4(kv[0], kv[1], kv[2], kv[3]);
+    kd[1] = make_float4(kv[4], kv[5], kv[6], kv[7]);
+    qd[0] = make_float4(qv[0], qv[1], qv[2], qv[3]);
+    qd[1] = make_float4(qv[4], qv[5], qv[6], qv[7]);
+    if (VG) {
+      float gv[8];
+      load_f32<8>(a.alpha + src, gv);
+      float4 *gd = reinterpret_cast<float4 *>(gs + j * DK + i);
+      gd[0] = make_float4(gv[0], gv[1], gv[2], gv[3]);
+      gd[1] = make_float4(gv[4], gv[5], gv[6], gv[7]);
+    }
   }
   for (int idx = lane; idx < n * kCols; idx += kWave) {
     const int j = idx / kCols, cc = idx % kCols;
@@ -112,12 +126,18 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   // (k, gate) and once per sequence (parent).
   if (tile == 0) {
     T *fk = static_cast<T *>(a.fk);
-    for (int idx = lane; idx < n * DK; idx += kWave) {
-      const int j = idx / DK, i = idx % DK;
+    constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte copy
+    for (int idx = lane; idx < n * (DK / E); idx += kWave) {
+      const int j = idx / (DK / E), i = (idx % (DK / E)) * E;
       const size_t s = (((size_t)b * n + j) * H + h) * DK + i;
-      fk[s] = k[s];
-      if (VG) a.falpha[s] = a.alpha[s];
+      *reinterpret_cast<uint4 *>(fk + s) = *reinterpret_cast<const uint4 *>(k + s);
     }
+    if (VG)
+      for (int idx = lane; idx < n * (DK / 4); idx += kWave) {
+        const int j = idx / (DK / 4), i = (idx % (DK / 4)) * 4;
+        const size_t s = (((size_t)b * n + j) * H + h) * DK + i;
+        *reinterpret_cast<float4 *>(a.falpha + s) = *reinterpret_cast<const float4 *>(a.alpha + s);
+      }
     if (lane < n) {
       const size_t s = ((size_t)b * n + lane) * H + h;
       if (!VG) a.falpha[s] = a.family == SLA_FAMILY_DELTANET ? 1.f : a.alpha[s];
