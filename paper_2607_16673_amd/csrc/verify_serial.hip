@@ -32,6 +32,7 @@ namespace {
 
 constexpr int kCols = 16;
 constexpr int kGroups = kWave / kCols;
+constexpr int kXcds = 8;  // workgroup i runs on XCD i mod 8
 
 // VG: per-key gates (GLA), staged on chip like the keys.
 template <int DK, typename T, bool CHAIN, bool VG>
@@ -42,11 +43,19 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   const int g = lane / kCols;
   const int H = a.H, dv = a.dv, n = a.n;
   const int ntiles = dv / kCols;
-  int w = blockIdx.x;
-  const int tile = w % ntiles;
-  w /= ntiles;
-  const int h = w % H;
-  const int b = w / H;
+  // neighbouring tiles (2m, 2m + 1) hold the two halves of each 128-byte row
+  // segment: their workgroups are numbered 8 apart, so that they run on the
+  // same XCD and share its L2 (consecutive workgroups go to different XCDs,
+  // whose L2s would each fetch and write back the whole lines)
+  const int npairs = (ntiles + 1) / 2;
+  const int x = blockIdx.x;
+  const int qd = x / kXcds;
+  const size_t pair = (size_t)(qd / 2) * kXcds + x % kXcds;
+  const int tile = 2 * (int)(pair % npairs) + qd % 2;
+  const size_t unit_id = pair / npairs;
+  if (tile >= ntiles || unit_id >= (size_t)a.B * H) return;  // padding of the numbering: no barrier follows
+  const int h = (int)(unit_id % H);
+  const int b = (int)(unit_id / H);
   const int col = tile * kCols + c;
   const int row0 = g * R;
   const size_t unit = (size_t)b * H + h;
@@ -257,7 +266,9 @@ hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const
 
 template <int DK, typename T>
 hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
-  const dim3 grid((unsigned)((size_t)a.B * a.H * (a.dv / kCols)));
+  // tile pairs numbered in groups of eight per XCD (see the kernel), padded to whole groups
+  const size_t pairs = (size_t)a.B * a.H * ((a.dv / kCols + 1) / 2);
+  const dim3 grid((unsigned)(((pairs + kXcds - 1) / kXcds) * 2 * kXcds));
   const bool vg = a.family == SLA_FAMILY_GLA;
   const size_t lds = serial_lds_bytes(a.n, DK, vg);
   if (vg) {
