@@ -288,7 +288,7 @@ def main():
             key += "/" + fam
         # counters taken on other library sources no longer describe this kernel
         from paper_2607_16673_amd.traffic import source_digest
-        if key in tj and tj[key].get("source_sha256") == source_digest("gdn"):
+        if key in tj and tj[key].get("source_sha256") == source_digest(tj[key].get("kernel", "verify_tile_kernel")):
             traffic = tj[key].get("bytes_per_launch")
             kernel = tj[key].get("kernel")
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -450,7 +450,7 @@ def run_conv(args, cfg, torch, B, inputs, dev):
             tj = json.load(f)
         key = "%s/conv/fused" % cfg.name
         from paper_2607_16673_amd.traffic import source_digest
-        if key in tj and tj[key].get("source_sha256") == source_digest("conv"):
+        if key in tj and tj[key].get("source_sha256") == source_digest(tj[key].get("kernel", "conv_verify_kernel")):
             line["roofline"]["traffic"] = tj[key].get("bytes_per_launch")
     if not args.no_cpu_baseline:
         log("bench: oracle CPU baseline (conv)")

@@ -38,18 +38,22 @@ KERNEL_TAG = "verify_tile_kernel"
 COPY_TAG = "mul"  # the elementwise multiply of run_copy (not the fill before it)
 
 
-# the sources each counted kernel is built from: counters taken on other
-# sources are stale
+# the sources each counted kernel is built from (with the host code that
+# chooses its launch): counters taken on other sources are stale
+_COMMON = ["device.hpp", "kernels.hpp", "api.cpp"]
 SOURCES = {
-    "gdn": ["verify_tile.hip", "verify_serial.hip", "decode.hip", "commit.hip", "device.hpp", "kernels.hpp"],
-    "conv": ["conv.hip", "device.hpp", "layer_ops.hpp"],
+    "verify_tile_kernel": ["verify_tile.hip"] + _COMMON,
+    "verify_serial_kernel": ["verify_serial.hip"] + _COMMON,
+    "decode_kernel": ["decode.hip"] + _COMMON,
+    "conv_verify_kernel": ["conv.hip", "device.hpp", "layer_ops.hpp", "api.cpp"],
+    "conv_node_kernel": ["conv.hip", "device.hpp", "layer_ops.hpp", "api.cpp"],
 }
 
 
-def source_digest(op: str = "gdn") -> str:
-    """sha256 over the sources of the kernels of one op (gdn or conv)."""
+def source_digest(kernel: str = KERNEL_TAG) -> str:
+    """sha256 over the sources of one counted kernel."""
     h = hashlib.sha256()
-    files = [os.path.join(HERE, "csrc", f) for f in SOURCES[op]]
+    files = [os.path.join(HERE, "csrc", f) for f in SOURCES[kernel]]
     for fn in files:
         with open(fn, "rb") as f:
             h.update(os.path.basename(fn).encode() + b"\0" + f.read())
@@ -127,7 +131,7 @@ def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, jso
         "fetch_kib_raw": round(bf, 1), "write_kib_raw": round(bw, 1),
         "copy_scale_fetch": round(scale_f, 4), "copy_scale_write": round(scale_w, 4),
         "dispatches": [nf, nw],
-        "source_sha256": source_digest("conv" if route == "conv" else "gdn"),
+        "source_sha256": source_digest(kernel),
     }
     data = {}
     if os.path.exists(json_path):
@@ -178,7 +182,7 @@ def summarize_mfma(out_dir: str, workload: str, skip: int, json_path: str, kerne
         "mfma_busy_cycles_per_simd": mean["SQ_VALU_MFMA_BUSY_CYCLES"] / simds,
         "bf16_mfma_flops": mean["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512,
         "gui_active_cycles_under_collection": mean["GRBM_GUI_ACTIVE"],
-        "source_sha256": source_digest("gdn"),
+        "source_sha256": source_digest(kernel),
     }
     data = {}
     if os.path.exists(json_path):
