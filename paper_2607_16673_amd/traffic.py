@@ -45,6 +45,7 @@ SOURCES = {
     "verify_tile_kernel": ["verify_tile.hip"] + _COMMON,
     "verify_serial_kernel": ["verify_serial.hip"] + _COMMON,
     "decode_kernel": ["decode.hip"] + _COMMON,
+    "commit_kernel": ["commit.hip"] + _COMMON,
     "conv_verify_kernel": ["conv.hip", "device.hpp", "layer_ops.hpp", "api.cpp"],
     "conv_node_kernel": ["conv.hip", "device.hpp", "layer_ops.hpp", "api.cpp"],
 }
