@@ -68,7 +68,10 @@ __global__ __launch_bounds__(kWave) void prune_kernel(PruneArgs a) {
   bool keep = inw;
   if (a.budget > 0 && __popcll(wmask) > a.budget) {
     int rank = 0;
-    for (int i = 0; i < n; ++i) {  // wave-uniform i: a register read, not a shuffle
+    // every lane i, unrolled (lanes past the window have no bit in wmask):
+    // wave-uniform i, so each step is a register read, not a shuffle
+#pragma unroll
+    for (int i = 0; i < kWave; ++i) {
       const float qi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(q), i));
       const bool wi = (wmask >> i) & 1ull;
       rank += (wi && (qi > q || (qi == q && i < l))) ? 1 : 0;
