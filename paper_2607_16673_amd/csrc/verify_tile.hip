@@ -15,7 +15,8 @@
 // own node's root path).  Only the committed state is read.
 //
 // One workgroup = one (batch b, head h) unit's V-tile of CW x 16 columns
-// (CW = 4 or 8), or TPW = 2 consecutive such tiles, with CW + 1 wavefronts:
+// (CW = 4 or 8), or TPW = 2 consecutive such tiles, with CW + 1 wavefronts
+// (CW = 4) or CW (CW = 8, where column wave 0 also takes the setup work):
 //   waves 0 .. CW-1 own 16 state columns each.  They issue the state tile
 //              reads (in the B-fragment order of v_mfma_f32_16x16x32_bf16: 8
 //              consecutive rows of one column per 32-row K-step) and the
@@ -32,7 +33,8 @@
 //              fragment is exactly the accumulator layout holding R, then U),
 //              and the outputs.  With two tiles, the second tile's reads go
 //              out once the first tile's registers are free.
-//   wave CW    owns no state.  It takes every read that depends on another
+//   wave CW    (the setup wave; wave 0 at CW = 8) owns no state of its own.
+//              It takes every read that depends on another
 //              read or that everything else waits for: parent row and gates
 //              -> topology, decays and compact-list offsets; the pending path
 //              with the previous round's parent row and gates -> validation;
@@ -150,15 +152,22 @@ constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
 // KIND: the family's form (see Layout).  Without the delta rule Lk = 0, so
 // T = I and U = R = V: no P_k, no Lk, no T.  WT: committed rows written
 // through at device scope (launches of one full round of workgroups).
+// eight column waves: column wave 0 also does the setup work, so that the
+// workgroup is eight waves and two fit a CU at 124 VGPRs (a ninth wave keeps
+// it to one: measured on 64-node trees at batch 64, d_v 256, 459 -> 448 us per
+// launch; its state reads then go out after its record gathers)
+template <int CW>
+constexpr int kWaves = CW == 8 ? CW : CW + 1;
+
 template <int DK, int NP, int CW, int TPW, int KIND, bool WT>
-__global__ __launch_bounds__((CW + 1) * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
+__global__ __launch_bounds__(kWaves<CW> * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
 void verify_tile_kernel(VerifyArgs a) {
   using L = Layout<DK, NP, CW, TPW, KIND>;
   constexpr bool DELTA = KIND == kKindDelta;
   constexpr bool GV = KIND == kKindGates;
   const bool nodelta = !DELTA || a.family == SLA_FAMILY_DECAY;  // R = V
   constexpr int kColWaves = CW;                 // waves 0 .. CW-1 own state columns
-  constexpr int kSetup = CW;                    // the setup wave
+  constexpr int kSetup = kWaves<CW> == CW ? 0 : CW;  // the setup wave
   constexpr int kTileCols = L::kTileCols;       // state columns per workgroup
   constexpr int KS = L::KS, NT = L::NT, MT = L::MT, CH = L::CH;
   constexpr int NGT = NT * (NT + 1);                        // Gram tiles (both halves)
@@ -236,7 +245,7 @@ void verify_tile_kernel(VerifyArgs a) {
     // and [Q; K] enter the memory queue ahead of the state (measured per
     // launch against no delay: 20 -> +1.6%, 40 -> -1.0%, 64 -> -1.7%,
     // 80 -> -2.1%, 100 -> -1.7%)
-    if (a.stagger) __builtin_amdgcn_s_sleep(80);
+    if (a.stagger && w != kSetup) __builtin_amdgcn_s_sleep(80);
     if (!a.late_state) load_state(t0, hfa);
     load_values(t0, vraw);
   }
@@ -351,7 +360,7 @@ void verify_tile_kernel(VerifyArgs a) {
   if (err != SLA_OK) return;
   // many rounds of workgroups: the state goes out only now, behind the small
   // reads the setup wave waits for
-  if (a.late_state && live(t0)) load_state(t0, hfa);
+  if (kSetup != 0 && a.late_state && live(t0)) load_state(t0, hfa);
   const int plen = s_misc[1];
 
   // ---- setup wave: records of the first kPMax path nodes, gathered straight
@@ -458,6 +467,9 @@ void verify_tile_kernel(VerifyArgs a) {
     }
     __syncthreads();
   }
+
+  // the folded setup wave's own state reads go out after its record gathers
+  if (kSetup == 0 && a.late_state && live(t0)) load_state(t0, hfa);
 
   // ---- tree-masked Grams over the column waves: tile (mr, na) of [Q; K] K^T holds
   //      rows of node tile mr % NT against ancestor candidates of node tile
@@ -843,7 +855,7 @@ hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
   // resident workgroups per CU for this instantiation (registers, LDS, waves)
   static const int per_cu = [&] {
     int k = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&k, kern_wb, (CW + 1) * kWave, lds) != hipSuccess || k < 1) k = 1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&k, kern_wb, kWaves<CW> * kWave, lds) != hipSuccess || k < 1) k = 1;
     return k;
   }();
   const size_t slots = (size_t)per_cu * device_cus();
@@ -852,7 +864,7 @@ hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
   // write-through only for a full round of workgroups that all stay resident:
   // below a round the launch is latency-bound and the writes' completion
   // lengthens it (batch 1, 32 workgroups: 8.6 -> 9.9 us per round)
-  hipLaunchKernelGGL(b.stagger ? kern_wt : kern_wb, dim3((unsigned)groups), dim3((CW + 1) * kWave), lds, s, b);
+  hipLaunchKernelGGL(b.stagger ? kern_wt : kern_wb, dim3((unsigned)groups), dim3(kWaves<CW> * kWave), lds, s, b);
   return hipGetLastError();
 }
 
