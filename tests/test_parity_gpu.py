@@ -160,6 +160,10 @@ LARGE = [
     inputs.Config("pair_tree13", 112, 64, 16, 128, 128, 13, False, 5, 3, inputs.BF16, 1),
     inputs.Config("pair_tree27_deep", 113, 64, 16, 128, 128, 27, False, 12, 3, inputs.BF16, 1),
     inputs.Config("pair_tree16_dv256", 114, 32, 16, 128, 256, 16, False, 5, 3, inputs.BF16, 1),
+    # 48-node trees at d_v 256: 128-column tiles, eight waves with the setup
+    # work on wave 0; 1024 workgroups are one full round at two per CU on a
+    # 256-CU part (state reads held back, committed rows written through)
+    inputs.Config("tree48_dv256_round", 115, 64, 16, 128, 256, 48, False, 8, 4, inputs.BF16, 1),
 ]
 
 
