@@ -34,14 +34,18 @@
 //              and the outputs.  With two tiles, the second tile's reads go
 //              out once the first tile's registers are free.
 //   wave CW    (the setup wave; wave 0 at CW = 8) owns no state of its own.
-//              It takes every read that depends on another
-//              read or that everything else waits for: parent row and gates
-//              -> topology, decays and compact-list offsets; the pending path
-//              with the previous round's parent row and gates -> validation;
-//              [Q; K] by direct global->LDS loads; then, while the column
-//              waves compute, the factor records the path names (also
-//              straight into LDS, a second stage for a second tile).  After
-//              the Grams it solves the per-node rows of T.
+//              It takes every read that depends on another read or that
+//              everything else waits for: parent row and gates -> topology,
+//              decays and compact-list offsets; the pending path with the
+//              previous round's parent row and gates -> validation; [Q; K] by
+//              direct global->LDS loads; then, while the column waves
+//              compute, the factor records the path names (also straight
+//              into LDS, a second stage for a second tile) and, for two
+//              16-node tiles with scalar gates, the second tile's first d_k/2
+//              state rows, which would otherwise queue behind the first
+//              tile's work (measured at batch 64, 16 heads, d_v 128: 37.8 ->
+//              36.9 us per launch).  After the Grams it solves the per-node
+//              rows of T.
 // The tree-masked Grams ([Q; K] K^T tiles that hold ancestor pairs, exact
 // bf16 products) run on the column waves; they and T are done while the
 // first tile's state is still in flight.  Strided global accesses go through
@@ -90,9 +94,17 @@ struct Layout {
   static constexpr int kXL = kGates ? kX : 0;       // low halves of [Q~; K~], same chunk layout
   static constexpr int kG = kGates ? NP * DK * 4 : 0;      // the draft's per-key gates
   static constexpr int kPg = kGates ? kPMax * DK * 4 : 0;  // pending per-key gates
+  // small trees, two 64-column tiles: the second tile's first DK/2 state rows
+  // are staged in LDS ahead of time (16-byte chunks, swizzled: see kernel).
+  // Not for GLA: its gate stages already take 37 KB at d_k 128, and 16 KB
+  // more would leave three resident workgroups per CU instead of four
+  // (measured 40.1 -> 43.4 us per launch at batch 64, 16 heads).
+  static constexpr bool kPrefetch = TPW == 2 && NP == 16 && CW == 4 && kDelta;
+  static constexpr int kPreInstr = kPrefetch ? (DK / 2) * (kTileCols / 4) / kWave : 0;  // 16-byte loads per lane
+  static constexpr int kPre = kPreInstr * kWave * 16;
   static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 4 + 16;
   static constexpr int oT = kX, oAt = oT + kT, oLk = oAt + kAt, oPk = oLk + kLk, oPu = oPk + kPk;
-  static constexpr int oXL = oPu + kPu, oG = oXL + kXL, oPg = oG + kG, oTopo = oPg + kPg;
+  static constexpr int oXL = oPu + kPu, oG = oXL + kXL, oPg = oG + kG, oPre = oPg + kPg, oTopo = oPre + kPre;
   static constexpr int kBytes = oTopo + kTopo;
 };
 
@@ -183,6 +195,7 @@ void verify_tile_kernel(VerifyArgs a) {
   uint4 *xl = reinterpret_cast<uint4 *>(lds + L::oXL);        // GLA: low halves of [Q~; K~]
   float *s_g = reinterpret_cast<float *>(lds + L::oG);        // GLA: [NP][DK] gates
   float *s_pg = reinterpret_cast<float *>(lds + L::oPg);      // GLA: [kPMax][DK] pending gates
+  float *s_pre = reinterpret_cast<float *>(lds + L::oPre);    // second tile's first DK/2 state rows
   unsigned char *tp = lds + L::oTopo;
   uint64_t *s_anc = reinterpret_cast<uint64_t *>(tp);      // [NP]
   int *s_depth = reinterpret_cast<int *>(tp + 8 * NP);     // [NP]
@@ -218,10 +231,10 @@ void verify_tile_kernel(VerifyArgs a) {
   // wave-uniform: this wave owns columns of tile t
   auto live = [&](int t) { return w < kColWaves && t * kTileCols + w * kWaveCols < dv; };
   // state rows 8 lg + e + 32 ks of column t * kTileCols + ucol, in B-fragment order
-  auto load_state = [&](int t, float (&hf)[KS][8]) {
+  auto load_state = [&](int t, float (&hf)[KS][8], int ks0 = 0) {
     const uint32_t sv = (uint32_t)(8 * lg * dv + t * kTileCols + ucol) * 4;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
+    for (int ks = ks0; ks < KS; ++ks)
 #pragma unroll
       for (int e = 0; e < 8; ++e) hf[ks][e] = buf_load_f32<kPolicyDefault>(sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
   };
@@ -402,6 +415,23 @@ void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
     for (int i = 0; i < TPW; ++i) gather_u(t0 + i, i);
   }
+  // ---- setup wave: the second tile's first DK/2 state rows into LDS, queued
+  //      behind the record gathers.  Chunk c holds row r = c / 16, column
+  //      chunk (c % 16) ^ 4 ((r / 8) % 4), so that the 16 column-wave lanes of
+  //      a row group and the four row groups fall on distinct banks.  Columns
+  //      past d_v (a ragged last tile) re-read column 0 and are never used.
+  if constexpr (L::kPrefetch) {
+    if (w == kSetup) {
+      const int cb = (t0 + 1) * kTileCols;
+#pragma unroll
+      for (int m = 0; m < L::kPreInstr; ++m) {
+        const int c = m * kWave + l;
+        const int r = c >> 4;
+        const int col = cb + 4 * ((c & 15) ^ (((r >> 3) & 3) << 2));
+        load_lds16(a.state + (unit * DK + r) * dv + (col < dv ? col : 0), s_pre + m * kWave * 4);
+      }
+    }
+  }
 
   // ---- GLA: Gamma_j = product of the gates over P(j) per key dimension, then
   //      Q~_j = Gamma_j * q_j and K~_j = k_j / Gamma_j split into bf16 hi (in
@@ -534,7 +564,8 @@ void verify_tile_kernel(VerifyArgs a) {
         }
       }
   }
-  if (w == kSetup) __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // the gathered records have landed
+  // the gathered records have landed (the staged state rows may still be in flight)
+  if (w == kSetup) __builtin_amdgcn_s_waitcnt(waitcnt_vm(L::kPreInstr));
   __syncthreads();
 
   if (DELTA && w == kSetup) {
@@ -737,10 +768,22 @@ void verify_tile_kernel(VerifyArgs a) {
     // and stores are computed: its state registers are free since the split,
     // its values since R
     if (TPW > 1 && more && live(t + 1)) {
-      load_state(t + 1, hn);
+      load_state(t + 1, hn, L::kPrefetch ? KS / 2 : 0);
       load_values(t + 1, vraw);
     }
+    if (L::kPrefetch && w == kSetup && i == 0) __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // staged rows landed
     __syncthreads();  // T complete
+    if (L::kPrefetch && more && live(t + 1)) {
+      // the staged rows of the next tile: row 32 ks + 8 lg + e, column chunk
+      // ucol / 4 swizzled by lg
+#pragma unroll
+      for (int ks = 0; ks < KS / 2; ++ks)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int r = ks * 32 + 8 * lg + e;
+          hn[ks][e] = s_pre[(r * 16 + ((ucol >> 2) ^ (lg << 2))) * 4 + (lc & 3)];
+        }
+    }
     // factor records independent of the V-tile -- k (from the staged rows),
     // alpha, parent -- while the column waves compute the first tile's
     // products (off the path to the barrier above)
