@@ -160,6 +160,11 @@ LARGE = [
     inputs.Config("pair_tree13", 112, 64, 16, 128, 128, 13, False, 5, 3, inputs.BF16, 1),
     inputs.Config("pair_tree27_deep", 113, 64, 16, 128, 128, 27, False, 12, 3, inputs.BF16, 1),
     inputs.Config("pair_tree16_dv256", 114, 32, 16, 128, 256, 16, False, 5, 3, inputs.BF16, 1),
+    # paired tiles whose second tile's first d_k/2 state rows are staged in
+    # LDS early: a ragged second tile (16 of its 64 columns inside d_v = 80),
+    # and d_k 64 (a half-size stage)
+    inputs.Config("pair_tree16_dv80", 116, 64, 32, 128, 80, 16, False, 5, 3, inputs.BF16, 1),
+    inputs.Config("pair_tree11_dk64", 117, 64, 16, 64, 128, 11, False, 4, 3, inputs.BF16, 1),
     # 48-node trees at d_v 256: 128-column tiles, eight waves with the setup
     # work on wave 0; 1024 workgroups are one full round at two per CU on a
     # 256-CU part (state reads held back, committed rows written through)
