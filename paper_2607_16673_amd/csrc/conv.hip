@@ -10,7 +10,8 @@
 // of §5.2 applied to C.
 //
 // One workgroup = one sequence b and a chunk of 512 channels, 8 per lane,
-// with up to four waves that split the draft's nodes.  Each wave first reads
+// with up to four waves (eight above 32 nodes) that split the draft's nodes.
+// Each wave first reads
 // the parent row into lanes (lane j holds node j), then issues its share of
 // the chunk's draft rows straight into LDS (global_load_lds_dwordx4: 16
 // bytes per lane, one instruction per bf16 row, two per fp32 row), and the
