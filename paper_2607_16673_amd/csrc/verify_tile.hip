@@ -2,7 +2,10 @@
 // the delayed state update of §5.2 fused in front of it.
 //
 // Unrolling the gated delta rule along a root path gives, for every node j
-// (gamma_j = product of alpha over P(j), D_ja = gamma_j / gamma_a, a in P(j)):
+// (gamma_j = product of alpha over P(j); for a in P(j), D_ja = product of
+// alpha over the nodes of P(j) strictly below a, which equals gamma_j /
+// gamma_a but is formed as a product, so no reciprocal of a decay product
+// is ever taken and strong decays underflow harmlessly to zero):
 //     H_j = gamma_j H0 + sum_{a in P(j)} D_ja k_a u_a^T
 //     (I + Lk) U = R,   R_j = beta_j (v_j - gamma_j H0^T k_j),
 //                       Lk_ja = beta_j D_ja (k_j . k_a)   for a in P(j), a != j
@@ -71,10 +74,12 @@ constexpr int kZ = 8;                             // root paths up to this depth
 //               R = V in place of beta (v - gamma P_k): a run-time choice,
 //               so that all three share one register allocation);
 //   kKindGates  GLA: one gate per key dimension, no delta rule.  The decay
-//               ratios become per-dimension, D_ja[i] = Gamma_j[i] / Gamma_a[i],
-//               and fold into the operands: Q~_j = Gamma_j * q_j and
-//               K~_a = k_a / Gamma_a (fp32, split into bf16 hi + lo), so
-//               Attn_ja = Q~_j . K~_a and O = Q~ H0 + Attn V.
+//               ratios become per-dimension, D_ja[i] (the product of the
+//               i-th gates of P(j) strictly below a), so the scores
+//               Attn_ja = sum_i q_j[i] D_ja[i] k_a[i] are formed on the
+//               vector ALUs by walking each root path, and
+//               O = Q~ H0 + Attn V with Q~_j = Gamma_j * q_j (fp32, split
+//               into bf16 hi + lo).
 constexpr int kKindDelta = 0, kKindGates = 1;
 
 template <int DK, int NP, int CW, int TPW, int KIND>
@@ -91,7 +96,7 @@ struct Layout {
   static constexpr int kLk = kDelta ? kList * 4 : 0;
   static constexpr int kPk = kPMax * DK * 2;        // pending keys (bf16)
   static constexpr int kPu = TPW * kPMax * kTileCols * 4;  // pending corrected values, one stage per tile
-  static constexpr int kXL = kGates ? kX : 0;       // low halves of [Q~; K~], same chunk layout
+  static constexpr int kXL = kGates ? kX / 2 : 0;   // low halves of Q~, same chunk layout
   static constexpr int kG = kGates ? NP * DK * 4 : 0;      // the draft's per-key gates
   static constexpr int kPg = kGates ? kPMax * DK * 4 : 0;  // pending per-key gates
   // small trees, two 64-column tiles: the second tile's first DK/2 state rows
@@ -102,7 +107,7 @@ struct Layout {
   static constexpr bool kPrefetch = TPW == 2 && NP == 16 && CW == 4 && kDelta;
   static constexpr int kPreInstr = kPrefetch ? (DK / 2) * (kTileCols / 4) / kWave : 0;  // 16-byte loads per lane
   static constexpr int kPre = kPreInstr * kWave * 16;
-  static constexpr int kTopo = NP * 8 + NP * 4 * 5 + kPMax * 4 + 16;
+  static constexpr int kTopo = NP * 8 + NP * 4 * 4 + kPMax * 4 + 16;
   static constexpr int oT = kX, oAt = oT + kT, oLk = oAt + kAt, oPk = oLk + kLk, oPu = oPk + kPk;
   static constexpr int oXL = oPu + kPu, oG = oXL + kXL, oPg = oG + kG, oPre = oPg + kPg, oTopo = oPre + kPre;
   static constexpr int kBytes = oTopo + kTopo;
@@ -156,10 +161,11 @@ __device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x
 }
 
 // Waves per SIMD the register allocation is held to: 6 (80 VGPRs) where the
-// tile state, accumulators and LDS allow a fourth resident workgroup per CU,
+// tile state, accumulators and LDS allow a fourth resident workgroup per CU;
+// 4 (128 VGPRs) for the eight-wave form, so that two workgroups fit a CU;
 // else whatever the allocation needs.
-template <int DK, int NP, int TPW>
-constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : 1;
+template <int DK, int NP, int CW>
+constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : (CW == 8 ? 4 : 1);
 
 // KIND: the family's form (see Layout).  Without the delta rule Lk = 0, so
 // T = I and U = R = V: no P_k, no Lk, no T.  WT: committed rows written
@@ -172,7 +178,7 @@ template <int CW>
 constexpr int kWaves = CW == 8 ? CW : CW + 1;
 
 template <int DK, int NP, int CW, int TPW, int KIND, bool WT>
-__global__ __launch_bounds__(kWaves<CW> * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, TPW>)))
+__global__ __launch_bounds__(kWaves<CW> * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, CW>)))
 void verify_tile_kernel(VerifyArgs a) {
   using L = Layout<DK, NP, CW, TPW, KIND>;
   constexpr bool DELTA = KIND == kKindDelta;
@@ -186,13 +192,13 @@ void verify_tile_kernel(VerifyArgs a) {
   constexpr int GT = (NGT + kColWaves - 1) / kColWaves;     // Gram tiles per column wave
 
   extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  uint4 *xs = reinterpret_cast<uint4 *>(lds);                 // [Q; K] (GLA: high halves of [Q~; K~])
+  uint4 *xs = reinterpret_cast<uint4 *>(lds);                 // [Q; K] (GLA: high halves of Q~ in place of Q)
   float *tb = reinterpret_cast<float *>(lds + L::oT);         // T blocks
   float *ab = reinterpret_cast<float *>(lds + L::oAt);        // Attn blocks
   float *lk = reinterpret_cast<float *>(lds + L::oLk);        // compact Lk
   bf16 *s_pk = reinterpret_cast<bf16 *>(lds + L::oPk);        // [kPMax][DK]
   float *s_pu = reinterpret_cast<float *>(lds + L::oPu);      // [kPMax][64]
-  uint4 *xl = reinterpret_cast<uint4 *>(lds + L::oXL);        // GLA: low halves of [Q~; K~]
+  uint4 *xl = reinterpret_cast<uint4 *>(lds + L::oXL);        // GLA: low halves of Q~
   float *s_g = reinterpret_cast<float *>(lds + L::oG);        // GLA: [NP][DK] gates
   float *s_pg = reinterpret_cast<float *>(lds + L::oPg);      // GLA: [kPMax][DK] pending gates
   float *s_pre = reinterpret_cast<float *>(lds + L::oPre);    // second tile's first DK/2 state rows
@@ -201,8 +207,7 @@ void verify_tile_kernel(VerifyArgs a) {
   int *s_depth = reinterpret_cast<int *>(tp + 8 * NP);     // [NP]
   int *s_off = s_depth + NP;                                // [NP]
   float *s_gamma = reinterpret_cast<float *>(s_off + NP);  // [NP]
-  float *s_rgamma = s_gamma + NP;                           // [NP] 1 / gamma
-  float *s_be = s_rgamma + NP;                              // [NP]
+  float *s_be = s_gamma + NP;                               // [NP]
   float *s_palpha = s_be + NP;                              // [kPMax]
   int *s_misc = reinterpret_cast<int *>(s_palpha + kPMax);  // err, path len
 
@@ -275,7 +280,7 @@ void verify_tile_kernel(VerifyArgs a) {
     const bool live = l < n;
     const size_t s = (nbase + (live ? l : 0)) * H + h;
     p = live ? a.parent[nbase + l] : -1;
-    // DeltaNet: no decay; GLA: the per-key gates enter through Q~ and K~
+    // DeltaNet: no decay; GLA: the per-key gates enter through Q~ and Attn
     al = (!GV && live && a.family != SLA_FAMILY_DELTANET) ? a.alpha[s] : 1.f;
     const float be = (DELTA && live && a.family != SLA_FAMILY_DECAY) ? a.beta[s] : 0.f;
     // pending accepted path, with the previous round's parent row and gates
@@ -314,15 +319,22 @@ void verify_tile_kernel(VerifyArgs a) {
     if (a.chain) bad = bad || (live && p != l - 1);
     int err = wave_any(bad) ? SLA_ERR_TOPOLOGY : SLA_OK;
     if (err == SLA_OK) {
+      // Walking up from j, g holds D_jx = product of the gates of P(j)
+      // strictly below x (j included) when the walk reaches ancestor x; the
+      // scalar families park it in the (not yet used) T block at (j, x) for
+      // the Grams.  Only products of gates: they may underflow, never
+      // overflow (no reciprocal of a decay product anywhere).
       uint64_t m = live ? (1ull << l) : 0ull;
       float g = al;
       int d = live ? 1 : 0;
       int x = p;
+      if (DELTA && live) tb[blk(l, l)] = 1.f;
       while (wave_any(x >= 0)) {
         const int src = x >= 0 ? x : 0;
         const float ax = __shfl(al, src);
         const int px = __shfl(p, src);
         if (x >= 0) {
+          if constexpr (DELTA) tb[blk(l, x)] = g;
           m |= 1ull << x;
           g *= ax;
           ++d;
@@ -343,7 +355,6 @@ void verify_tile_kernel(VerifyArgs a) {
         s_depth[l] = d;
         s_off[l] = incl - d;
         s_gamma[l] = g;
-        s_rgamma[l] = 1.f / g;
         s_be[l] = be;
       }
     }
@@ -364,6 +375,7 @@ void verify_tile_kernel(VerifyArgs a) {
     if (l == 0) {
       s_misc[0] = err;
       s_misc[1] = plen;
+      s_misc[2] = maxd;
     }
     if (t0 == 0 && h == 0 && l == 0 && a.status) a.status[b] = err;
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));  // [Q; K] has landed
@@ -433,65 +445,111 @@ void verify_tile_kernel(VerifyArgs a) {
     }
   }
 
-  // ---- GLA: Gamma_j = product of the gates over P(j) per key dimension, then
-  //      Q~_j = Gamma_j * q_j and K~_j = k_j / Gamma_j split into bf16 hi (in
-  //      place of q_j, k_j) + lo; one lane per (node, 4 key dimensions).  The
-  //      records (the key as given, the gates) are written from here.
+  // ---- GLA: the tree-masked scores with per-key decay ratios,
+  //          Attn_ja = sum_i q_j[i] D_ja[i] k_a[i],  D_ja = product of the
+  //          gates of P(j) strictly below a (j included), per key dimension,
+  //      on the vector ALUs: 16 lanes per node j, each holding d_k / 16 key
+  //      dimensions of qc = D_ja * q_j.  Walking up P(j) from j, every step
+  //      sums qc . k_a over the 16 lanes (DPP) and then multiplies in a's
+  //      gates, so qc ends as Gamma_j * q_j = Q~_j, split into bf16 hi (in
+  //      place of q_j) + lo for P_q = Q~ H0.  Gate products only: they may
+  //      underflow, never overflow.  The records (the key as given, the
+  //      gates) are written from here.
   if constexpr (GV) {
     if (w < kColWaves) {
-      constexpr int C4 = DK / 4;
+      constexpr int E = DK / 16;  // key dimensions per lane
+      const int maxd = s_misc[2];
       unsigned char *xb = reinterpret_cast<unsigned char *>(xs);
       unsigned char *xlb = reinterpret_cast<unsigned char *>(xl);
-      for (int it = w * kWave + l; it < NP * C4; it += kColWaves * kWave) {
-        const int j = it / C4, c4 = it % C4;
-        const int oq = xchunk<CH>(j, c4 >> 1) * 16 + (c4 & 1) * 8;
-        const int ok = xchunk<CH>(NP + j, c4 >> 1) * 16 + (c4 & 1) * 8;
-        if (j >= n) {  // padding rows: zero low halves (their products are masked or dropped)
-          *reinterpret_cast<uint2 *>(xlb + oq) = make_uint2(0, 0);
-          *reinterpret_cast<uint2 *>(xlb + ok) = make_uint2(0, 0);
+      // byte offset of the 4 (E = 4) or 8 key dimensions d0 .. of stage row r
+      auto xoff = [&](int r, int d0) { return xchunk<CH>(r, d0 >> 3) * 16 + ((d0 >> 2) & 1) * 8; };
+      auto load_row = [&](int r, int d0, float (&x)[E]) {
+#pragma unroll
+        for (int c = 0; c < E; c += 8 < E ? 8 : E) {
+          uint32_t wv[4];
+          if constexpr (E >= 8) {
+            const uint4 u = *reinterpret_cast<const uint4 *>(xb + xoff(r, d0 + c));
+            wv[0] = u.x, wv[1] = u.y, wv[2] = u.z, wv[3] = u.w;
+          } else {
+            const uint2 u = *reinterpret_cast<const uint2 *>(xb + xoff(r, d0 + c));
+            wv[0] = u.x, wv[1] = u.y;
+          }
+#pragma unroll
+          for (int e = 0; e < (E >= 8 ? 8 : E); e += 2) {
+            x[c + e] = __uint_as_float(wv[e / 2] << 16);
+            x[c + e + 1] = __uint_as_float(wv[e / 2] & 0xffff0000u);
+          }
+        }
+      };
+      // the sum over the 16 lanes of a DPP row, in every lane
+      auto row_sum = [](float v) {
+        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0xB1, 0xF, 0xF, false));   // quad_perm 1,0,3,2
+        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x4E, 0xF, 0xF, false));   // quad_perm 2,3,0,1
+        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x141, 0xF, 0xF, false));  // row_half_mirror
+        v += __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x140, 0xF, 0xF, false));  // row_mirror
+        return v;
+      };
+#pragma unroll 1
+      for (int it0 = w * kWave; it0 < NP * 16; it0 += kColWaves * kWave) {  // wave-uniform
+        const int j = (it0 + l) >> 4, d0 = ((it0 + l) & 15) * E;
+        const bool first = (l & 15) == 0;
+        float qc[E];
+        load_row(j, d0, qc);  // padding rows hold node 0's query
+        uint64_t rest = j < n ? s_anc[j] : 0ull;
+        // every lane takes all maxd steps, so the DPP rows stay whole
+#pragma unroll 1
+        for (int st = 0; st < maxd; ++st) {
+          const bool act = rest != 0ull;
+          const int an = act ? 63 - __builtin_clzll(rest) : 0;  // deepest ancestor left: j, then up
+          rest &= ~(1ull << an);
+          float ka[E];
+          load_row(NP + an, d0, ka);
+          float sdot = 0.f;
+#pragma unroll
+          for (int e = 0; e < E; ++e) sdot = __builtin_fmaf(qc[e], ka[e], sdot);
+          sdot = row_sum(sdot);
+          if (act && first) ab[blk(j, an)] = sdot;
+          if (act) {
+#pragma unroll
+            for (int e = 0; e < E; e += 4) {
+              const float4 gx = *reinterpret_cast<const float4 *>(s_g + an * DK + d0 + e);
+              qc[e] *= gx.x;
+              qc[e + 1] *= gx.y;
+              qc[e + 2] *= gx.z;
+              qc[e + 3] *= gx.w;
+            }
+          }
+        }
+        if (j >= n) {  // padding rows: zero low halves (their products are dropped)
+#pragma unroll
+          for (int c = 0; c < E; c += 4) *reinterpret_cast<uint2 *>(xlb + xoff(j, d0 + c)) = make_uint2(0, 0);
           continue;
         }
-        float G[4] = {1.f, 1.f, 1.f, 1.f};
-        for (uint64_t m = s_anc[j]; m; m &= m - 1ull) {
-          const float4 gx = *reinterpret_cast<const float4 *>(s_g + __builtin_ctzll(m) * DK + 4 * c4);
-          G[0] *= gx.x;
-          G[1] *= gx.y;
-          G[2] *= gx.z;
-          G[3] *= gx.w;
-        }
-        const uint2 qb = *reinterpret_cast<const uint2 *>(xb + oq);
-        const uint2 kb = *reinterpret_cast<const uint2 *>(xb + ok);
-        const uint32_t qw[2] = {qb.x, qb.y}, kw[2] = {kb.x, kb.y};
-        uint32_t qh[2], ql[2], kh[2], kl[2];
 #pragma unroll
-        for (int e2 = 0; e2 < 2; ++e2) {
-          uint32_t hq = 0, lq = 0, hk = 0, lk2 = 0;
+        for (int c = 0; c < E; c += 4) {
+          uint32_t hw[2], lw[2];
 #pragma unroll
-          for (int s2 = 0; s2 < 2; ++s2) {
-            const int e = 2 * e2 + s2;
-            const float qf = __uint_as_float((s2 ? qw[e2] >> 16 : qw[e2] & 0xffffu) << 16) * G[e];
-            const float kf = __uint_as_float((s2 ? kw[e2] >> 16 : kw[e2] & 0xffffu) << 16) / G[e];
-            const __bf16 qhi = static_cast<__bf16>(qf), khi = static_cast<__bf16>(kf);
-            const __bf16 qlo = static_cast<__bf16>(qf - static_cast<float>(qhi));
-            const __bf16 klo = static_cast<__bf16>(kf - static_cast<float>(khi));
-            hq |= (uint32_t)__builtin_bit_cast(uint16_t, qhi) << (16 * s2);
-            lq |= (uint32_t)__builtin_bit_cast(uint16_t, qlo) << (16 * s2);
-            hk |= (uint32_t)__builtin_bit_cast(uint16_t, khi) << (16 * s2);
-            lk2 |= (uint32_t)__builtin_bit_cast(uint16_t, klo) << (16 * s2);
+          for (int e2 = 0; e2 < 2; ++e2) {
+            uint32_t hv = 0, lv = 0;
+#pragma unroll
+            for (int s2 = 0; s2 < 2; ++s2) {
+              const float x = qc[c + 2 * e2 + s2];
+              const __bf16 xh = static_cast<__bf16>(x);
+              const __bf16 xl2 = static_cast<__bf16>(x - static_cast<float>(xh));
+              hv |= (uint32_t)__builtin_bit_cast(uint16_t, xh) << (16 * s2);
+              lv |= (uint32_t)__builtin_bit_cast(uint16_t, xl2) << (16 * s2);
+            }
+            hw[e2] = hv;
+            lw[e2] = lv;
           }
-          qh[e2] = hq;
-          ql[e2] = lq;
-          kh[e2] = hk;
-          kl[e2] = lk2;
-        }
-        *reinterpret_cast<uint2 *>(xb + oq) = make_uint2(qh[0], qh[1]);
-        *reinterpret_cast<uint2 *>(xlb + oq) = make_uint2(ql[0], ql[1]);
-        *reinterpret_cast<uint2 *>(xb + ok) = make_uint2(kh[0], kh[1]);
-        *reinterpret_cast<uint2 *>(xlb + ok) = make_uint2(kl[0], kl[1]);
-        if (t0 == 0) {
-          const size_t r = ((nbase + j) * H + h) * DK + 4 * c4;
-          *reinterpret_cast<uint2 *>(static_cast<bf16 *>(a.fk) + r) = kb;
-          *reinterpret_cast<float4 *>(a.falpha + r) = *reinterpret_cast<const float4 *>(s_g + j * DK + 4 * c4);
+          *reinterpret_cast<uint2 *>(xb + xoff(j, d0 + c)) = make_uint2(hw[0], hw[1]);
+          *reinterpret_cast<uint2 *>(xlb + xoff(j, d0 + c)) = make_uint2(lw[0], lw[1]);
+          if (t0 == 0) {
+            const size_t r = ((nbase + j) * H + h) * DK + d0 + c;
+            *reinterpret_cast<uint2 *>(static_cast<bf16 *>(a.fk) + r) =
+                *reinterpret_cast<const uint2 *>(xb + xoff(NP + j, d0 + c));
+            *reinterpret_cast<float4 *>(a.falpha + r) = *reinterpret_cast<const float4 *>(s_g + j * DK + d0 + c);
+          }
         }
       }
     }
@@ -501,10 +559,11 @@ void verify_tile_kernel(VerifyArgs a) {
   // the folded setup wave's own state reads go out after its record gathers
   if (kSetup == 0 && a.late_state && live(t0)) load_state(t0, hfa);
 
-  // ---- tree-masked Grams over the column waves: tile (mr, na) of [Q; K] K^T holds
-  //      rows of node tile mr % NT against ancestor candidates of node tile
-  //      na <= mr % NT; ancestor entries go to Attn blocks and Lk lists
-  {
+  // ---- tree-masked Grams over the column waves (scalar gates; GLA's scores
+  //      were formed above): tile (mr, na) of [Q; K] K^T holds rows of node
+  //      tile mr % NT against ancestor candidates of node tile na <= mr % NT;
+  //      ancestor entries go to Attn blocks and Lk lists
+  if constexpr (!GV) {
     f32x4 gacc[GT];
     int tc = 0;
 #pragma unroll
@@ -518,12 +577,6 @@ void verify_tile_kernel(VerifyArgs a) {
           const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mr * 16 + lc, ks * 4 + lg));
           const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
           g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, g, 0, 0, 0);
-          if constexpr (GV) {  // Q~ K~^T = hi hi + hi lo + lo hi
-            const bf16x8 al8 = *reinterpret_cast<const bf16x8 *>(xl + xchunk<CH>(mr * 16 + lc, ks * 4 + lg));
-            const bf16x8 bl8 = *reinterpret_cast<const bf16x8 *>(xl + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
-            g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bl8, g, 0, 0, 0);
-            g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al8, bf, g, 0, 0, 0);
-          }
         }
         gacc[tc / kColWaves] = g;
       }
@@ -538,25 +591,24 @@ void verify_tile_kernel(VerifyArgs a) {
         const int an = na * 16 + lc;
         const int jb = (mr % NT) * 16 + 4 * lg;
         uint32_t anc[4];  // the half of row j's ancestor mask that holds column an
-        float gj[4], bj[4];
+        float dj[4], bj[4];  // dj: decay ratio D_{j,an}, parked in the T block (j, an)
         int oj[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           anc[q] = reinterpret_cast<const uint32_t *>(s_anc)[2 * (jb + q) + (na >> 1)];
-          gj[q] = s_gamma[jb + q];
+          dj[q] = tb[blk(jb + q, an)];  // an <= 16 (jb / 16) + 15: inside the block row
           if (mr >= NT) {
             bj[q] = s_be[jb + q];
             oj[q] = s_off[jb + q];
           }
         }
-        const float ra = s_rgamma[an];
         const int da = mr >= NT ? s_depth[an] : 0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int j = jb + q;
           // rows past the last node hold stale LDS words: masked by j < n
           if (j >= n || an > j || (mr >= NT && an == j) || !((anc[q] >> (an & 31)) & 1u)) continue;
-          const float dg = gj[q] * ra * gacc[tc / kColWaves][q];
+          const float dg = dj[q] * gacc[tc / kColWaves][q];
           if (mr < NT)
             ab[blk(j, an)] = dg;
           else
@@ -788,7 +840,7 @@ void verify_tile_kernel(VerifyArgs a) {
     // alpha, parent -- while the column waves compute the first tile's
     // products (off the path to the barrier above)
     if (w == kSetup && i == 0 && t0 == 0) {
-      if constexpr (!GV) {  // GLA's key and gate records went out with Q~, K~
+      if constexpr (!GV) {  // GLA's key and gate records went out with Q~
         bf16 *fk = static_cast<bf16 *>(a.fk);
         for (int c = l; c < n * CH; c += kWave) {
           const int j = c / CH, part = c % CH;

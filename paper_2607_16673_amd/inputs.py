@@ -16,6 +16,9 @@ proposal trees of the paper's evaluation, §8, which are not available):
     beta only, the scalar-decay family alpha only (both as above); GLA's
     per-key gates are g = sigmoid(z)^(1/16), z ~ N(0, 1) per (layer, b,
     node, head, key dimension), fp32 (GLA's gate with its normaliser 16);
+  * strong-forgetting gates for the near-reset edge case: alpha (or each of
+    GLA's per-key gates) ~ U(1e-3, 0.3), with about 3% set to 1e-6 and 2% to
+    1e-20;
   * chains: parent[j] = j - 1; trees: node 0 is the root, node i > 0 picks a
     uniform parent among earlier nodes whose depth and child count are still
     below the configured limits;
@@ -232,6 +235,22 @@ def family_gates(cfg: Config, rnd, layer_pos: int, family: str, layer: int | Non
     if family == "gla":
         return draw_gla_gates(cfg, layer_pos if layer is None else layer, round_index, batch), None
     raise ValueError(family)
+
+
+def draw_strong_gates(cfg: Config, layer: int, round_index: int = 0, batch: int | None = None,
+                      family: str = "gdn") -> np.ndarray:
+    """Strong-forgetting gates (the near-reset edge of a gated state):
+    alpha ~ U(1e-3, 0.3), with about 3% of the gates set to 1e-6 and 2% to
+    1e-20; [B][n][H] fp32, or [B][n][H][dk] per-key gates for "gla".  Along
+    a root path their products leave the fp32 range within a few nodes."""
+    B = cfg.batch if batch is None else batch
+    shape = (B, cfg.n_nodes, cfg.heads) + ((cfg.d_k,) if family == "gla" else ())
+    rng = _rng(base_seed(cfg), round_index, 7, layer)
+    g = rng.uniform(1e-3, 0.3, shape)
+    u = rng.uniform(0.0, 1.0, shape)
+    g[u < 0.03] = 1e-6
+    g[(u >= 0.03) & (u < 0.05)] = 1e-20
+    return g.astype(np.float32)
 
 
 def draw_state(cfg: Config, layer: int, batch: int | None = None) -> np.ndarray:
