@@ -65,7 +65,7 @@ extern "C" {
 #define SLA_TOPO_TREE 0
 #define SLA_TOPO_CHAIN 1
 
-/* Verification route.
+/* Verification route (sla_shape.route).
  *   AUTO      the library chooses from the topology hint and the shape:
  *             1-node drafts (the decode step) take a streaming kernel of
  *             their own (whole-line state passes, two column sums); bf16
@@ -113,6 +113,8 @@ typedef struct sla_shape {
   int32_t qkv_dtype; /* SLA_DTYPE_F32 or SLA_DTYPE_BF16                     */
   int32_t topology;  /* SLA_TOPO_TREE or SLA_TOPO_CHAIN                     */
   int32_t family;    /* SLA_FAMILY_*; 0 (GDN) when zero-initialised         */
+  int32_t route;     /* SLA_ROUTE_* for sla_verify; 0 (AUTO) when
+                        zero-initialised; ignored by sla_commit            */
 } sla_shape;
 
 /* Factor store (§5.1, factor buffering).  One record per node and head:
@@ -174,15 +176,18 @@ typedef struct sla_pending {
  *   out     device fp32 [B][n][H][d_v]; o_j = S_j q_j.
  *   factors device factor store written for this draft (see sla_factors).
  *   status  device int32 [B] or NULL: 0, SLA_ERR_TOPOLOGY or SLA_ERR_PATH.
- *   route   SLA_ROUTE_*.  Both routes stage the draft on chip.  With GLA's
- *           per-key gates the parallel route holds d_k = 256 drafts of up
- *           to 32 nodes (PARALLEL: SLA_ERR_UNSUPPORTED above; AUTO then takes
- *           SERIAL), and the serial route d_k = 256 drafts of up to 50 nodes
- *           (SLA_ERR_UNSUPPORTED above).  Gates (alpha, GLA's g) lie in
- *           (0, 1]; the parallel route divides by their products along a
- *           root path, which must stay within the fp32 normal range.
+ * The route is shape->route (SLA_ROUTE_*; an unknown value is
+ * SLA_ERR_SHAPE).  Every route stages the draft on chip.  With GLA's
+ * per-key gates the parallel route holds d_k = 256 drafts of up to 32 nodes
+ * (PARALLEL: SLA_ERR_UNSUPPORTED above; AUTO then takes SERIAL), and the
+ * serial route d_k = 256 drafts of up to 50 nodes (SLA_ERR_UNSUPPORTED
+ * above).  Gates (alpha, GLA's g) lie in (0, 1]; every route only
+ * multiplies them (decay ratios along a root path are products of the gates
+ * between the two nodes), so any gate in that range, however small, is
+ * valid: strong decays underflow towards zero as they do in exact
+ * arithmetic.
  * Returns SLA_OK once the work is enqueued, or a negative error code. */
-int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pending *pending,
+int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
                const void *q, const void *k, const void *v, const float *alpha,
                const float *beta, const int32_t *parent_idx, float *out,
                const sla_factors *factors, int32_t *status, hipStream_t stream);

@@ -54,7 +54,7 @@ TOPOLOGIES = {"tree": SLA_TOPO_TREE, "chain": SLA_TOPO_CHAIN}
 class SlaShape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("heads", ctypes.c_int32), ("d_k", ctypes.c_int32),
                 ("d_v", ctypes.c_int32), ("n_nodes", ctypes.c_int32), ("qkv_dtype", ctypes.c_int32),
-                ("topology", ctypes.c_int32), ("family", ctypes.c_int32)]
+                ("topology", ctypes.c_int32), ("family", ctypes.c_int32), ("route", ctypes.c_int32)]
 
 
 class SlaFactors(ctypes.Structure):
@@ -94,7 +94,7 @@ def lib():
             raise RuntimeError("libsla.so is not built (run `python -m paper_2607_16673_amd.build`)")
         L = ctypes.CDLL(LIB_PATH)
         vp, i32 = ctypes.c_void_p, ctypes.c_int32
-        L.sla_verify.argtypes = [ctypes.POINTER(SlaShape), i32, vp, ctypes.POINTER(SlaPending),
+        L.sla_verify.argtypes = [ctypes.POINTER(SlaShape), vp, ctypes.POINTER(SlaPending),
                                  vp, vp, vp, vp, vp, vp, vp, ctypes.POINTER(SlaFactors), vp, vp]
         L.sla_verify.restype = ctypes.c_int
         L.sla_commit.argtypes = [ctypes.POINTER(SlaShape), vp, ctypes.POINTER(SlaFactors), vp, vp, vp, vp]
@@ -156,10 +156,11 @@ def sla_validate_path_host(parent, path, length) -> int:
     return lib().sla_validate_path_host(p.ctypes.data, len(p), pa.ctypes.data, int(length))
 
 
-def make_shape(batch, heads, d_k, d_v, n_nodes, dtype="bf16", topology="tree", family="gdn") -> SlaShape:
+def make_shape(batch, heads, d_k, d_v, n_nodes, dtype="bf16", topology="tree", family="gdn",
+               route="auto") -> SlaShape:
     return SlaShape(int(batch), int(heads), int(d_k), int(d_v), int(n_nodes),
                     SLA_DTYPE_BF16 if dtype == "bf16" else SLA_DTYPE_F32, TOPOLOGIES[topology],
-                    FAMILIES[family])
+                    FAMILIES[family], ROUTES[route] if isinstance(route, str) else int(route))
 
 
 def gate_shape(batch, n, heads, d_k, family="gdn") -> tuple:
@@ -247,7 +248,7 @@ def sla_verify(state, q, k, v, alpha, beta, parent_idx, out, factors: Factors, *
     B, n, H, dk = q.shape
     dv = v.shape[-1]
     dt = _dtype_code(q)
-    shape = SlaShape(B, H, dk, dv, n, dt, TOPOLOGIES[topology], FAMILIES[family])
+    shape = SlaShape(B, H, dk, dv, n, dt, TOPOLOGIES[topology], FAMILIES[family], ROUTES[route])
     f = factors.c(q.dtype, B, n, H, dk, dv, family)
     pend_p = None
     if pending is not None:
@@ -259,7 +260,7 @@ def sla_verify(state, q, k, v, alpha, beta, parent_idx, out, factors: Factors, *
         pend_p = ctypes.byref(pend)
     st_p = _dev(status, torch.int32, (B,), "status") if status is not None else None
     code = lib().sla_verify(
-        ctypes.byref(shape), ROUTES[route], _dev(state, torch.float32, (B, H, dk, dv), "state"), pend_p,
+        ctypes.byref(shape), _dev(state, torch.float32, (B, H, dk, dv), "state"), pend_p,
         _dev(q, q.dtype, (B, n, H, dk), "q"), _dev(k, q.dtype, (B, n, H, dk), "k"),
         _dev(v, q.dtype, (B, n, H, dv), "v"),
         _dev(alpha, torch.float32, gate_shape(B, n, H, dk, family), "alpha") if alpha is not None else None,
@@ -274,7 +275,7 @@ def sla_commit(state, factors: Factors, path, length, *, status=None, family: st
     torch = _torch()
     B, n, H, dk = factors.k.shape
     dv = factors.u.shape[-1]
-    shape = SlaShape(B, H, dk, dv, n, _dtype_code(factors.k), SLA_TOPO_TREE, FAMILIES[family])
+    shape = SlaShape(B, H, dk, dv, n, _dtype_code(factors.k), SLA_TOPO_TREE, FAMILIES[family], SLA_ROUTE_AUTO)
     f = factors.c(factors.k.dtype, B, n, H, dk, dv, family)
     st_p = _dev(status, torch.int32, (B,), "status") if status is not None else None
     code = lib().sla_commit(ctypes.byref(shape), _dev(state, torch.float32, (B, H, dk, dv), "state"),

@@ -14,7 +14,7 @@
 
 namespace {
 
-constexpr int kVersion = 10000;  // 1.0.0
+constexpr int kVersion = 20000;  // 2.0.0: the route moved into sla_shape
 
 bool dk_ok(int dk) { return dk == 64 || dk == 128 || dk == 256; }
 
@@ -36,7 +36,7 @@ bool overlaps(Range a, Range b) { return a.lo < b.hi && b.lo < a.hi; }
 int check_shape(const sla_shape *s) {
   if (!s) return SLA_ERR_NULL;
   if (s->batch < 1 || s->heads < 1 || s->n_nodes < 1 || s->n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
-  if (s->d_k < 1 || s->d_v < 16 || s->d_v > 4096 || s->d_v % 16 != 0) return SLA_ERR_SHAPE;
+  if (s->d_k < 1 || s->d_v < 16 || s->d_v > 1024 || s->d_v % 16 != 0) return SLA_ERR_SHAPE;
   if (s->qkv_dtype != SLA_DTYPE_F32 && s->qkv_dtype != SLA_DTYPE_BF16) return SLA_ERR_DTYPE;
   if (s->topology != SLA_TOPO_TREE && s->topology != SLA_TOPO_CHAIN) return SLA_ERR_SHAPE;
   if (s->family < SLA_FAMILY_GDN || s->family > SLA_FAMILY_GLA) return SLA_ERR_SHAPE;
@@ -110,13 +110,14 @@ size_t sla_factors_bytes(const sla_shape *shape) {
   return f.k + f.u + f.alpha + f.parent;
 }
 
-int sla_verify(const sla_shape *shape, int32_t route, float *state, const sla_pending *pending,
+int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
                const void *q, const void *k, const void *v, const float *alpha, const float *beta,
                const int32_t *parent_idx, float *out, const sla_factors *factors, int32_t *status,
                hipStream_t stream) {
   int st = check_shape(shape);
   if (st != SLA_OK) return st;
   const int fam = shape->family;
+  const int route = shape->route;
   if (!state || !q || !k || !v || (reads_alpha(fam) && !alpha) || (reads_beta(fam) && !beta) || !parent_idx ||
       !out || !factors_complete(factors))
     return SLA_ERR_NULL;

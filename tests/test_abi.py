@@ -117,7 +117,9 @@ def _verify(shape, route=0, pending=None, nulls=(), factors=None):
     for i in nulls:
         args[i] = None
     f = factors or B.SlaFactors(_ptr(10), _ptr(11), _ptr(12), _ptr(13))
-    return B.lib().sla_verify(ctypes.byref(shape) if shape is not None else None, route, args[0],
+    if shape is not None:
+        shape.route = route
+    return B.lib().sla_verify(ctypes.byref(shape) if shape is not None else None, args[0],
                               ctypes.byref(pending) if pending is not None else None,
                               args[1], args[2], args[3], args[4], args[5], args[6], args[7],
                               ctypes.byref(f), None, None)
@@ -163,7 +165,8 @@ def test_verify_rejects_pending_aliasing_output_factors():
     # misaligned state pointer
     args = [ctypes.c_void_p(FAKE + 4)] + [_ptr(i) for i in range(1, 9)]
     f = B.SlaFactors(_ptr(10), _ptr(11), _ptr(12), _ptr(13))
-    assert B.lib().sla_verify(ctypes.byref(ok), 0, args[0], None, *args[1:8], ctypes.byref(f),
+    ok.route = 0
+    assert B.lib().sla_verify(ctypes.byref(ok), args[0], None, *args[1:8], ctypes.byref(f),
                               None, None) == B.SLA_ERR_UNSUPPORTED
 
 
@@ -176,9 +179,10 @@ def test_family_argument_rules_return_before_launch():
 
     def call(family, alpha, beta, state=None, route=0, shape=None):
         s = shape or B.make_shape(2, 4, 128, 128, 8, "bf16", family=family)
+        s.route = route
         args = [state or _ptr(0)] + [_ptr(i) for i in range(1, 9)]
         args[4], args[5] = alpha, beta
-        return L.sla_verify(ctypes.byref(s), route, args[0], None, *args[1:8], ctypes.byref(f), None, None)
+        return L.sla_verify(ctypes.byref(s), args[0], None, *args[1:8], ctypes.byref(f), None, None)
 
     mis = ctypes.c_void_p(FAKE + 4)
     # DeltaNet: beta required, alpha not read
