@@ -66,33 +66,79 @@ def graph_plan(steps, layers, max_launches=48):
     return g, k // g
 
 
-def cpu_baseline(cfg, rounds, states, budget_s=10.0, gates=None, family="gdn"):
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), or the platform's."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or platform.machine()
+
+
+def _oracle_pass(oracle, cfg, r0, states, gates, family, layer, seqs=None):
+    """One verify + commit of one layer of round r0 by the oracle, over all
+    sequences or the first `seqs`."""
+    sl = slice(None) if seqs is None else slice(0, seqs)
+    a, b = gates[layer] if gates is not None else (r0.alpha[layer], r0.beta[layer])
+    a = a[sl] if a is not None else None
+    b = b[sl] if b is not None else None
+    out, st = oracle.verify(states[layer][sl], r0.q32[layer][sl], r0.k32[layer][sl], r0.v32[layer][sl], a, b,
+                            r0.parent[sl], family=family)
+    S1, st2 = oracle.commit(states[layer][sl], r0.k32[layer][sl], r0.v32[layer][sl], a, b, r0.parent[sl],
+                            r0.path[sl], r0.length[sl], family=family)
+    assert (st == 0).all() and (st2 == 0).all()
+
+
+def cpu_baseline(cfg, rounds, states, budget_s=10.0, gates=None, family="gdn", single_s=4.0, single_seqs=4):
     """The fp64 oracle (verify + commit by definition) on the host cores, on
     whole layers of the same workload, cycling through the layers until about
-    budget_s of CPU time has passed.  gates: per layer (alpha, beta) inputs of
-    the family."""
+    budget_s of CPU time has passed; then single-threaded on a subset (the
+    first `single_seqs` sequences of each layer, all heads) for about
+    single_s.  gates: per layer (alpha, beta) inputs of the family."""
     import oracle
 
     r0 = rounds
+    threads = oracle.num_threads()
+    # one untimed pass first: the first touches of the fp64 working arrays
+    # (page faults) are not the oracle's arithmetic
+    _oracle_pass(oracle, cfg, r0, states, gates, family, 0)
     t0 = time.perf_counter()
     passes = 0
     while True:
-        layer = passes % cfg.layers
-        a, b = gates[layer] if gates is not None else (r0.alpha[layer], r0.beta[layer])
-        out, st = oracle.verify(states[layer], r0.q32[layer], r0.k32[layer], r0.v32[layer], a, b, r0.parent,
-                                family=family)
-        S1, st2 = oracle.commit(states[layer], r0.k32[layer], r0.v32[layer], a, b, r0.parent, r0.path,
-                                r0.length, family=family)
-        assert (st == 0).all() and (st2 == 0).all()
+        _oracle_pass(oracle, cfg, r0, states, gates, family, passes % cfg.layers)
         passes += 1
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = time.perf_counter() - t0
     nodes = passes * cfg.batch * cfg.n_nodes
-    return {"value": nodes / dt, "unit": "nodes/s", "cores": oracle.num_threads(), "kind": "oracle",
+    # one thread on a subset: the same per-node work, so the rates compare
+    seqs = min(single_seqs, cfg.batch)
+    oracle.set_num_threads(1)
+    try:
+        t1 = time.perf_counter()
+        sp = 0
+        while True:
+            _oracle_pass(oracle, cfg, r0, states, gates, family, sp % cfg.layers, seqs=seqs)
+            sp += 1
+            if time.perf_counter() - t1 >= single_s:
+                break
+        dt1 = time.perf_counter() - t1
+    finally:
+        oracle.set_num_threads(threads)
+    single = sp * seqs * cfg.n_nodes / dt1
+    return {"value": round(nodes / dt, 1), "unit": "nodes/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(),
             "sample": "%d layer passes over the %d layers of the %s workload (all %d sequences x %d heads each), "
-                      "verify + commit of one round, %.1f s" % (passes, cfg.layers, cfg.name, cfg.batch,
-                                                                 cfg.heads, dt)}
+                      "verify + commit of one round, %.1f s on %d threads" % (passes, cfg.layers, cfg.name, cfg.batch,
+                                                                               cfg.heads, dt, threads),
+            "single_thread": {"value": round(single, 1), "unit": "nodes/s",
+                              "sample": "%d layer passes over the first %d sequences (x %d heads) of each layer, "
+                                        "verify + commit, %.1f s on 1 thread" % (sp, seqs, cfg.heads, dt1)},
+            "thread_scaling": round((nodes / dt) / single, 2)}
 
 
 def main():
@@ -108,6 +154,11 @@ def main():
     ap.add_argument("--separate", action="store_true",
                     help="time the separate route (verify, then standalone commit) instead of the fused one")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extra", action="store_true",
+                    help="default run only: skip the other batch >= 64 workloads (64-node trees and the 1-node "
+                         "decode chain at batch 256)")
+    ap.add_argument("--no-copy-ceiling", action="store_true",
+                    help="default run only: skip the measured copy ceiling")
     ap.add_argument("--no-graph", dest="graph", action="store_false",
                     help="launch eagerly from Python with HIP events around every launch")
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
@@ -117,10 +168,12 @@ def main():
                          "top-k trees at the paper's target shape (8 heads, d_k = d_v = 256, batch 1); "
                          "fused-commit: fused commit-and-verify vs verify plus standalone commit for accepted "
                          "lengths 1..8 at verify length 4 (the same shape)")
-    ap.add_argument("--op", default="gdn", choices=["gdn", "conv", "prune"],
+    ap.add_argument("--op", default="gdn", choices=["gdn", "conv", "prune", "commit"],
                     help="gdn: the recurrent-state verify+commit (the headline); conv: the layer's short "
                          "causal convolution with its conv-state commit, on the same drafts; prune: draft "
-                         "pruning and packing of 64-candidate rollouts down to the workload's tree size")
+                         "pruning and packing of 64-candidate rollouts down to the workload's tree size; "
+                         "commit: the standalone accepted-path commit alone, over rotating states of at least "
+                         "1.5 GiB in total (cold: no verification of the same state right before it)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -149,6 +202,151 @@ def main():
         return run_conv(args, cfg, torch, B, inputs, dev)
     if args.op == "prune":
         return run_prune(args, cfg, torch, B, inputs, dev)
+    if args.op == "commit":
+        return run_commit(args, cfg, torch, B, inputs, dev)
+    res = time_gdn(args, cfg, torch, B, inputs, dev, steps=args.steps, warmup=args.warmup,
+                   keep_inputs=not args.no_cpu_baseline)
+    fam = args.family
+    topo = "chain" if cfg.chain else "tree"
+    traffic, kernel = lookup_traffic(args, cfg, fam)
+    roof = {"bound": "hbm", "achieved": round(res["achieved"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(res["achieved"] / HBM_PEAK_GBS, 4), "traffic": traffic,
+            "kernel": kernel or ("sla verify (%s route)%s" % (args.route, " + sla commit" if args.separate else "")),
+            "algorithmic_bytes_per_launch": int(res["bytes_launch"]), "avg_launch_ms": round(res["v_ms"], 5)}
+    line = {
+        "metric": METRIC, "value": round(res["value"], 1), "unit": "nodes/s", "n_gpus": 1, "steps": res["steps"],
+        "warmup": args.warmup, "ms_per_step": round(res["ms_per_step"], 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        # bf16 q/k/v (the paper's activation precision) against an fp32 state
+        # and fp32 gates; the contractions run on the matrix cores with the
+        # fp32 operands split into bf16 hi + lo parts, accumulated in fp32
+        "dtype": "bf16 q/k/v, f32 state" if cfg.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.batch, "heads": cfg.heads, "d_k": cfg.d_k,
+                   "d_v": cfg.d_v, "nodes_per_tree": cfg.n_nodes, "topology": topo,
+                   "max_depth": cfg.max_depth, "max_branch": cfg.max_branch, "layers": cfg.layers,
+                   "qkv_dtype": cfg.dtype, "state_dtype": "f32", "route": args.route,
+                   "commit": "separate" if args.separate else "fused", "family": fam,
+                   "parallelism": "single-gpu",
+                   "launch": "hip graph" if args.graph else "eager"},
+        "hbm_gbps": round(res["achieved"], 1),
+        # one token through every layer of the workload (one layer's node is `value`'s unit)
+        "tokens_per_s": round(res["tokens_per_s"], 1),
+        "roofline": roof,
+    }
+    if res.get("c_ms") is not None:
+        line["commit_avg_launch_ms"] = round(res["c_ms"], 5)
+    default_run = (args.workload == DEFAULT_WORKLOAD and fam == "gdn" and args.route == "auto"
+                   and not args.separate and args.graph)
+    if default_run and not args.no_copy_ceiling:
+        log("bench: copy ceiling")
+        cc = copy_ceiling(torch, dev)
+        line["copy_ceiling"] = cc
+        roof["frac_of_copy_ceiling"] = round(res["achieved"] / cc["gbps"], 4)
+    if default_run and not args.no_extra:
+        # the other batch >= 64 workloads: 64-node trees and the 1-node decode
+        # chain at batch 256 (one layer each, same fused route)
+        extra = {}
+        for name in EXTRA_WORKLOADS:
+            xc = inputs.config(name)
+            r = time_gdn(args, xc, torch, B, inputs, dev, steps=20, warmup=args.warmup, keep_inputs=False)
+            t, _ = lookup_traffic(args, xc, fam)
+            e = {"nodes_per_s": round(r["value"], 1), "avg_launch_ms": round(r["v_ms"], 5),
+                 "algorithmic_bytes_per_launch": int(r["bytes_launch"]), "achieved_gbps": round(r["achieved"], 1),
+                 "frac": round(r["achieved"] / HBM_PEAK_GBS, 4), "traffic": t, "steps": r["steps"],
+                 "config": {"batch": xc.batch, "heads": xc.heads, "d_k": xc.d_k, "d_v": xc.d_v,
+                            "nodes_per_tree": xc.n_nodes, "topology": "chain" if xc.chain else "tree",
+                            "max_depth": xc.max_depth, "max_branch": xc.max_branch, "layers": xc.layers}}
+            if "copy_ceiling" in line:
+                e["frac_of_copy_ceiling"] = round(r["achieved"] / line["copy_ceiling"]["gbps"], 4)
+            extra[name] = e
+            log("bench: %s %.1f us per launch, %.1f GB/s (%.1f%% of 8 TB/s)"
+                % (name, r["v_ms"] * 1e3, r["achieved"], 100 * r["achieved"] / HBM_PEAK_GBS))
+            del r
+            torch.cuda.empty_cache()
+        line["workloads_batch_ge_64"] = extra
+    if not args.no_cpu_baseline:
+        log("bench: oracle CPU baseline")
+        line["cpu_baseline"] = cpu_baseline(cfg, res["rnd"], res["states_np"], gates=res["gates"], family=fam)
+    print(json.dumps(line), flush=True)
+
+
+EXTRA_WORKLOADS = ["large_batch_tree64", "large_batch_chain1"]
+
+
+def lookup_traffic(args, cfg, fam):
+    """(HBM bytes per launch from the counters, counted kernel) for this
+    workload, or (None, None) when none were taken on the current sources."""
+    if not os.path.exists(args.traffic_json):
+        return None, None
+    with open(args.traffic_json) as f:
+        tj = json.load(f)
+    key = "%s/%s/%s" % (cfg.name, args.route, "separate" if args.separate else "fused")
+    if fam != "gdn":
+        key += "/" + fam
+    # counters taken on other library sources no longer describe this kernel
+    from paper_2607_16673_amd.traffic import source_digest
+    if key in tj and tj[key].get("source_sha256") == source_digest(tj[key].get("kernel", "verify_tile_kernel")):
+        return tj[key].get("bytes_per_launch"), tj[key].get("kernel")
+    return None, None
+
+
+def copy_ceiling(torch, dev, total_bytes=3 << 30, buffers=6, reps=5):
+    """A measured ceiling for streaming the state: plain copies (torch's
+    elementwise copy) and in-place read-modify-write passes (torch's x *= 1)
+    over `buffers` rotating fp32 buffers of total_bytes / buffers each, far
+    beyond the 256 MB last-level cache, launched back to back from a HIP
+    graph.  GB/s counts every byte read and written once."""
+    n = total_bytes // buffers // 4
+    src = [torch.empty(n, dtype=torch.float32, device=dev).normal_() for _ in range(buffers)]
+    dst = [torch.empty_like(x) for x in src]
+
+    def span(launch):
+        launch()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        sc = torch.cuda.Stream(dev)
+        sc.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(sc):
+            with torch.cuda.graph(g, stream=sc):
+                launch()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        cur = torch.cuda.current_stream(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(cur)
+        for _ in range(reps):
+            g.replay()
+        e1.record(cur)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * buffers)  # ms per buffer pass
+
+    def copy_all():
+        for d, x in zip(dst, src):
+            d.copy_(x)
+
+    def rmw_all():
+        for x in src:
+            x.mul_(1.0)
+
+    t_copy = span(copy_all)
+    t_rmw = span(rmw_all)
+    per = n * 4 * 2
+    g_copy = per / (t_copy * 1e-3) / 1e9
+    g_rmw = per / (t_rmw * 1e-3) / 1e9
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"gbps": round(max(g_copy, g_rmw), 1), "copy_gbps": round(g_copy, 1), "in_place_rmw_gbps": round(g_rmw, 1),
+            "frac_of_peak": round(max(g_copy, g_rmw) / HBM_PEAK_GBS, 4), "bytes_per_pass": int(per),
+            "kernel": "torch elementwise copy_ and in-place mul_(1.0), %d rotating %d MiB fp32 buffers, HIP graph"
+                      % (buffers, n * 4 >> 20)}
+
+
+def time_gdn(args, cfg, torch, B, inputs, dev, steps, warmup, keep_inputs=True):
+    """Time `steps` speculative rounds of one GDN workload (per layer one fused
+    commit-and-verify, or with --separate a verify then a standalone commit).
+    Returns a dict of measurements (and the host inputs when keep_inputs)."""
+    fam = args.family
     topo = "chain" if cfg.chain else "tree"
     log("bench: generating %s (%d layers)" % (cfg.name, cfg.layers))
     rnd = inputs.draw_round(cfg, 0)
@@ -160,7 +358,6 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
 
     adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
-    fam = args.family
     gates = [inputs.family_gates(cfg, rnd, l, fam, layer=l) for l in range(cfg.layers)]
 
     def dev_or_none(x):
@@ -207,8 +404,8 @@ def main():
                 events[-1].record(stream)
         step_no[0] += 1
 
-    log("bench: warmup %d" % args.warmup)
-    for _ in range(max(args.warmup, 2)):
+    log("bench: warmup %d" % warmup)
+    for _ in range(max(warmup, 2)):
         step()
     torch.cuda.synchronize()
     assert int(status.abs().max()) == 0, "device reported a data error"
@@ -217,7 +414,7 @@ def main():
         # One graph holds an even number of consecutive steps (the factor
         # stores ping-pong), replayed back to back: no host work between
         # kernel launches.
-        gsteps, reps = graph_plan(args.steps, cfg.layers)
+        gsteps, reps = graph_plan(steps, cfg.layers)
         if step_no[0] % 2:
             step()
         g = torch.cuda.CUDAGraph()
@@ -250,7 +447,6 @@ def main():
         vdur = [e0.elapsed_time(e1) / (steps * cfg.layers)]
         cdur = []
     else:
-        steps = args.steps
         log("bench: timing %d steps" % steps)
         events = []
         torch.cuda.synchronize()
@@ -278,46 +474,12 @@ def main():
         bytes_launch += cfg.batch * cfg.heads * cfg.d_k * cfg.d_v * 4
     achieved = bytes_launch / (v_ms * 1e-3) / 1e9
     nodes = cfg.batch * cfg.n_nodes * cfg.layers * steps
-    value = nodes / elapsed
-    traffic = None
-    kernel = None
-    if os.path.exists(args.traffic_json):
-        with open(args.traffic_json) as f:
-            tj = json.load(f)
-        key = "%s/%s/%s" % (cfg.name, args.route, "separate" if args.separate else "fused")
-        if fam != "gdn":
-            key += "/" + fam
-        # counters taken on other library sources no longer describe this kernel
-        from paper_2607_16673_amd.traffic import source_digest
-        if key in tj and tj[key].get("source_sha256") == source_digest(tj[key].get("kernel", "verify_tile_kernel")):
-            traffic = tj[key].get("bytes_per_launch")
-            kernel = tj[key].get("kernel")
-    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-            "kernel": kernel or ("sla verify (%s route)%s" % (args.route, " + sla commit" if args.separate else "")),
-            "algorithmic_bytes_per_launch": int(bytes_launch), "avg_launch_ms": round(v_ms, 5)}
-    line = {
-        "metric": METRIC, "value": round(value, 1), "unit": "nodes/s", "n_gpus": 1, "steps": steps,
-        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": cfg.name, "batch": cfg.batch, "heads": cfg.heads, "d_k": cfg.d_k,
-                   "d_v": cfg.d_v, "nodes_per_tree": cfg.n_nodes, "topology": topo,
-                   "max_depth": cfg.max_depth, "max_branch": cfg.max_branch, "layers": cfg.layers,
-                   "qkv_dtype": cfg.dtype, "state_dtype": "f32", "route": args.route,
-                   "commit": "separate" if args.separate else "fused", "family": fam,
-                   "parallelism": "single-gpu",
-                   "launch": "hip graph" if args.graph else "eager"},
-        "hbm_gbps": round(achieved, 1),
-        # one token through every layer of the workload (one layer's node is `value`'s unit)
-        "tokens_per_s": round(cfg.batch * cfg.n_nodes * steps / elapsed, 1),
-        "roofline": roof,
-    }
-    if cdur:
-        line["commit_avg_launch_ms"] = round(float(np.mean(cdur)), 5)
-    if not args.no_cpu_baseline:
-        log("bench: oracle CPU baseline")
-        line["cpu_baseline"] = cpu_baseline(cfg, rnd, states_np, gates=gates, family=fam)
-    print(json.dumps(line), flush=True)
+    res = {"value": nodes / elapsed, "steps": steps, "ms_per_step": ms_per_step, "v_ms": v_ms,
+           "c_ms": float(np.mean(cdur)) if cdur else None, "bytes_launch": bytes_launch, "achieved": achieved,
+           "tokens_per_s": cfg.batch * cfg.n_nodes * steps / elapsed}
+    if keep_inputs:
+        res.update(rnd=rnd, states_np=states_np, gates=gates)
+    return res
 
 
 def conv_algorithmic_bytes(cfg, D, K, pending_len, n_prev):
@@ -456,6 +618,92 @@ def run_conv(args, cfg, torch, B, inputs, dev):
     if not args.no_cpu_baseline:
         log("bench: oracle CPU baseline (conv)")
         line["cpu_baseline"] = conv_cpu_baseline(cfg, (parent_np, path_np, length_np), xs32, Cs, ws)
+    print(json.dumps(line), flush=True)
+
+
+def run_commit(args, cfg, torch, B, inputs, dev, min_bytes=3 << 29):
+    """Timed standalone commits (sla_commit) of the workload's accepted
+    paths, one per state, over max(layers, enough states for min_bytes)
+    rotating states, so that no state is in the last-level cache when its
+    commit starts and none was just read by a verification.  The factor
+    records come from one untimed verification per state."""
+    state_bytes = cfg.batch * cfg.heads * cfg.d_k * cfg.d_v * 4
+    nst = max(cfg.layers, -(-min_bytes // state_bytes))
+    fam = args.family
+    log("bench: generating %s (%d rotating states of %d MiB)" % (cfg.name, nst, state_bytes >> 20))
+    rnd = inputs.draw_round(cfg, 0, layers=[0])
+    adt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+
+    def act(x):
+        if cfg.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    a_np, b_np = inputs.family_gates(cfg, rnd, 0, fam, layer=0)
+    q, k, v = act(rnd.q[0]), act(rnd.k[0]), act(rnd.v[0])
+    a = torch.from_numpy(a_np).to(dev) if a_np is not None else None
+    bt = torch.from_numpy(b_np).to(dev) if b_np is not None else None
+    parent = torch.from_numpy(rnd.parent).to(dev)
+    path = torch.from_numpy(rnd.path).to(dev)
+    length = torch.from_numpy(rnd.length).to(dev)
+    S0 = torch.from_numpy(inputs.draw_state(cfg, 0)).to(dev)
+    states = [S0.clone() for _ in range(nst)]
+    del S0
+    f = B.Factors.empty(cfg.batch, cfg.n_nodes, cfg.heads, cfg.d_k, cfg.d_v, adt, dev, family=fam)
+    out = torch.empty(cfg.batch, cfg.n_nodes, cfg.heads, cfg.d_v, dtype=torch.float32, device=dev)
+    status = torch.zeros(cfg.batch, dtype=torch.int32, device=dev)
+    B.sla_verify(states[0], q, k, v, a, bt, parent, out, f, status=status,
+                 topology="chain" if cfg.chain else "tree", family=fam)
+
+    def step():
+        for st in states:
+            B.sla_commit(st, f, path, length, status=status, family=fam)
+
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    assert int(status.abs().max()) == 0, "device reported a data error"
+    reps = max(1, args.steps)
+    g = torch.cuda.CUDAGraph()
+    s_cap = torch.cuda.Stream(dev)
+    s_cap.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(s_cap):
+        with torch.cuda.graph(g, stream=s_cap):
+            step()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    cur = torch.cuda.current_stream(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(cur)
+    for _ in range(reps):
+        g.replay()
+    e1.record(cur)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert int(status.abs().max()) == 0, "device reported a data error"
+    c_ms = e0.elapsed_time(e1) / (reps * nst)
+    w = 2 if cfg.dtype == "bf16" else 4
+    gate = cfg.d_k * 4 if fam == "gla" else 4
+    A = int(np.sum(rnd.length))
+    bytes_launch = (2 * state_bytes + A * cfg.heads * (cfg.d_k * w + cfg.d_v * 4 + gate)
+                    + cfg.batch * cfg.n_nodes * 4 * 2 + cfg.batch * 4)
+    achieved = bytes_launch / (c_ms * 1e-3) / 1e9
+    line = {
+        "metric": "accepted-path commits/sec (standalone, cold states)",
+        "value": round(cfg.batch * reps * nst / elapsed, 1), "unit": "sequence-layers/s", "n_gpus": 1,
+        "steps": reps, "warmup": args.warmup, "ms_per_step": round(1e3 * elapsed / reps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32 state",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "op": "standalone commit", "batch": cfg.batch, "heads": cfg.heads,
+                   "d_k": cfg.d_k, "d_v": cfg.d_v, "rotating_states": nst, "state_mib": state_bytes >> 20,
+                   "mean_accepted": round(float(np.mean(rnd.length)), 3), "family": fam,
+                   "parallelism": "single-gpu", "launch": "hip graph"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None, "kernel": "commit_kernel",
+                     "algorithmic_bytes_per_launch": int(bytes_launch), "avg_launch_ms": round(c_ms, 5)},
+    }
     print(json.dumps(line), flush=True)
 
 

@@ -46,6 +46,7 @@ def _load():
         _b.build()
     lib = ctypes.CDLL(_LIB_PATH)
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_gdn_step.argtypes = [ctypes.c_int, ctypes.c_int, _dp, _dp, _dp,
                                     ctypes.c_double, ctypes.c_double, _dp]
     lib.oracle_readout.argtypes = [ctypes.c_int, ctypes.c_int, _dp, _dp, _dp]
@@ -89,6 +90,12 @@ def _p(a, t):
 def num_threads() -> int:
     """Threads the oracle's OpenMP loops use (OMP_NUM_THREADS or all cores)."""
     return _load().oracle_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """Threads for the following calls (timing only; results are identical
+    for any count)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def gdn_step(Hs, k, v, alpha, beta):

@@ -66,6 +66,16 @@ int oracle_num_threads(void) {
 #endif
 }
 
+/* Threads for the following parallel loops (timing only; results do not
+ * depend on it: every unit is computed by one thread, in the same order). */
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n > 0) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 /* One GDN step on H = S^T ([dk][dv]).  kH is caller scratch of length dv.
  *   kH[c]   = sum_i k[i] H[i][c]                       (the row k^T H)
  *   H[i][c] = alpha*(H[i][c] - beta*k[i]*kH[c]) + beta*k[i]*v[c]          */
