@@ -77,10 +77,19 @@ extern "C" {
  *   PARALLEL  tree-masked factorised verification (§4.2): one dense
  *             contraction of all queries and keys with the committed state
  *             on the matrix cores, then a tree-masked triangular solve for
- *             the corrected values and a tree-masked readout.            */
+ *             the corrected values and a tree-masked readout.
+ *   HYBRID    chain-decomposed verification (§4.3): the draft is split by
+ *             heavy-light decomposition into node-disjoint chains, each
+ *             verified by the serial per-node loop; chains whose boundary
+ *             state (the state of the chain head's parent) is ready run in
+ *             parallel, level by level.  The boundary state is rebuilt on
+ *             chip from the committed state and the ancestors' factor
+ *             records.  Bitwise equal to SERIAL.  A CHAIN draft is a single
+ *             chain and runs as SERIAL.                                  */
 #define SLA_ROUTE_AUTO 0
 #define SLA_ROUTE_SERIAL 1
 #define SLA_ROUTE_PARALLEL 2
+#define SLA_ROUTE_HYBRID 3
 
 #define SLA_MAX_NODES 64
 
@@ -180,8 +189,8 @@ typedef struct sla_pending {
  * SLA_ERR_SHAPE).  Every route stages the draft on chip.  With GLA's
  * per-key gates the parallel route holds d_k = 256 drafts of up to 32 nodes
  * (PARALLEL: SLA_ERR_UNSUPPORTED above; AUTO then takes SERIAL), and the
- * serial route d_k = 256 drafts of up to 50 nodes (SLA_ERR_UNSUPPORTED
- * above).  Gates (alpha, GLA's g) lie in (0, 1]; every route only
+ * serial and hybrid routes d_k = 256 drafts of up to 50 nodes
+ * (SLA_ERR_UNSUPPORTED above).  Gates (alpha, GLA's g) lie in (0, 1]; every route only
  * multiplies them (decay ratios along a root path are products of the gates
  * between the two nodes), so any gate in that range, however small, is
  * valid: strong decays underflow towards zero as they do in exact

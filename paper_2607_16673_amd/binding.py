@@ -36,6 +36,7 @@ SLA_TOPO_CHAIN = 1
 SLA_ROUTE_AUTO = 0
 SLA_ROUTE_SERIAL = 1
 SLA_ROUTE_PARALLEL = 2
+SLA_ROUTE_HYBRID = 3
 SLA_MAX_NODES = 64
 SLA_FAMILY_GDN = 0
 SLA_FAMILY_DELTANET = 1
@@ -47,7 +48,8 @@ SLA_ACT_NONE = 0
 SLA_ACT_SILU = 1
 SLA_CONV_MAX_KERNEL = 4
 
-ROUTES = {"auto": SLA_ROUTE_AUTO, "serial": SLA_ROUTE_SERIAL, "parallel": SLA_ROUTE_PARALLEL}
+ROUTES = {"auto": SLA_ROUTE_AUTO, "serial": SLA_ROUTE_SERIAL, "parallel": SLA_ROUTE_PARALLEL,
+          "hybrid": SLA_ROUTE_HYBRID}
 TOPOLOGIES = {"tree": SLA_TOPO_TREE, "chain": SLA_TOPO_CHAIN}
 
 

@@ -121,7 +121,8 @@ int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
   if (!state || !q || !k || !v || (reads_alpha(fam) && !alpha) || (reads_beta(fam) && !beta) || !parent_idx ||
       !out || !factors_complete(factors))
     return SLA_ERR_NULL;
-  if (route != SLA_ROUTE_AUTO && route != SLA_ROUTE_SERIAL && route != SLA_ROUTE_PARALLEL) return SLA_ERR_SHAPE;
+  if (route != SLA_ROUTE_AUTO && route != SLA_ROUTE_SERIAL && route != SLA_ROUTE_PARALLEL && route != SLA_ROUTE_HYBRID)
+    return SLA_ERR_SHAPE;
   if (pending) {
     if (!factors_complete(&pending->f) || !pending->path || !pending->len) return SLA_ERR_NULL;
     if (pending->n_nodes < 1 || pending->n_nodes > SLA_MAX_NODES) return SLA_ERR_SHAPE;
@@ -148,7 +149,7 @@ int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
   if (route == SLA_ROUTE_PARALLEL) {
     if (!parallel_ok) return SLA_ERR_UNSUPPORTED;
     use_parallel = true;
-  } else if (route == SLA_ROUTE_SERIAL) {
+  } else if (route == SLA_ROUTE_SERIAL || route == SLA_ROUTE_HYBRID) {
     use_parallel = false;
   } else {
     // bf16 drafts, chains included, go to the tree-masked contraction on the
@@ -192,6 +193,8 @@ int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
   hipError_t e;
   if (route == SLA_ROUTE_AUTO && shape->n_nodes == 1)  // the decode step: its own streaming kernel
     e = sla::launch_verify_decode(a, shape->qkv_dtype, stream);
+  else if (route == SLA_ROUTE_HYBRID)
+    e = sla::launch_verify_hybrid(a, shape->qkv_dtype, stream);
   else
     e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)
                      : sla::launch_verify_serial(a, shape->qkv_dtype, stream);

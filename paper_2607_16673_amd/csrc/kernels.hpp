@@ -66,6 +66,8 @@ struct TopologyArgs {
 // Each launcher returns hipSuccess or the launch error.  `dtype` is
 // SLA_DTYPE_F32 or SLA_DTYPE_BF16.
 hipError_t launch_verify_serial(const VerifyArgs &a, int dtype, hipStream_t s);
+// chain-decomposed hybrid (chains run through the serial kernel)
+hipError_t launch_verify_hybrid(const VerifyArgs &a, int dtype, hipStream_t s);
 bool parallel_supported(int dk, int dv, int n, int dtype);
 hipError_t launch_verify_parallel(const VerifyArgs &a, int dtype, hipStream_t s);
 // 1-node drafts (a.n == 1), any family and activation dtype

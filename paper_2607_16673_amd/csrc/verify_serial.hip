@@ -1,7 +1,8 @@
-// verify_serial.hip -- state-resident serial verification (SpecLA §4.1),
-// with the delayed state update of §5.2 fused in front of it.
+// verify_serial.hip -- state-resident verification (SpecLA §4.1) and the
+// chain-decomposed hybrid schedule built on it (§4.3), with the delayed state
+// update of §5.2 fused in front of both.
 //
-// One wavefront owns one (batch b, head h, 16-column V-tile) slice of the
+// A wavefront owns one (batch b, head h, 16-column V-tile) slice of the
 // transposed state H = S^T: the full d_k rows of 16 value columns (V-dimension
 // tiling keeps every output column local, §4.1 "Tiling").  Lane (g, c) holds
 // column c of the contiguous row block g*R .. g*R+R-1 (R = d_k / 4) in
@@ -18,21 +19,55 @@
 // DeltaNet with alpha = 1; the no-delta families (scalar decay, GLA) with
 // u_j = v_j; GLA's per-key gates g_j scale row i by g_j[i] in place of
 // alpha_j, so b_j = H_par^T (g_j * q_j) and H_j = diag(g_j) H_par + k_j u_j^T.
-// Nodes are visited in DFS pre-order; a chain therefore advances the
-// registers in place.  When the next node's parent is
+//
+// Serial route: one wave per slice visits the nodes in DFS pre-order; a chain
+// therefore advances the registers in place.  When the next node's parent is
 // not the state in registers (a branch point of a tree), that state is
-// rebuilt from the committed tile kept in registers by re-applying the
-// stored factors of the parent's root path -- rank-one updates only, the
-// reductions of shared prefixes are never repeated.
-#include "device.hpp"
-#include "kernels.hpp"
+// rebuilt from the committed tile kept in registers by re-applying the stored
+// factors of the parent's root path -- rank-one updates only, the reductions
+// of shared prefixes are never repeated.
+//
+// Hybrid route: the draft is split by heavy-light decomposition into
+// node-disjoint chains (each node continues the chain of its parent when it
+// is the parent's child with the largest subtree, ties to the smaller index;
+// every other node starts a chain).  The chains are verified by the same
+// per-node loop, one wave per chain, several waves per slice; a chain's level
+// is the number of chain starts strictly above its head, and the chains of
+// one level run in parallel once every shallower level is done (a workgroup
+// barrier per level).  A chain's boundary state -- the state of its head's
+// parent -- is materialised on chip from the committed tile and the rank-one
+// factor records of the head's ancestors, which the shallower chains left in
+// LDS; no boundary state goes to memory.  Every node's state is the committed
+// tile advanced by the records of its root path in root-first order, on both
+// routes, so the serial and hybrid routes agree bit for bit.
+#include "serial_stage.hpp"
 
 namespace sla {
 namespace {
 
-constexpr int kCols = 16;
+constexpr int kCols = kSliceCols;
 constexpr int kGroups = kWave / kCols;
 constexpr int kXcds = 8;  // workgroup i runs on XCD i mod 8
+
+// Slice numbering shared by both kernels: neighbouring tiles (2m, 2m + 1)
+// hold the two halves of each 128-byte row segment; their workgroups are
+// numbered 8 apart, so that they run on the same XCD and share its L2
+// (consecutive workgroups go to different XCDs, whose L2s would each fetch
+// and write back the whole lines).  Returns false for the padding of the
+// numbering.
+__device__ inline bool slice_of(const VerifyArgs &a, int &tile, int &b, int &h) {
+  const int ntiles = a.dv / kCols;
+  const int npairs = (ntiles + 1) / 2;
+  const int x = blockIdx.x;
+  const int qd = x / kXcds;
+  const size_t pair = (size_t)(qd / 2) * kXcds + x % kXcds;
+  tile = 2 * (int)(pair % npairs) + qd % 2;
+  const size_t unit_id = pair / npairs;
+  if (tile >= ntiles || unit_id >= (size_t)a.B * a.H) return false;
+  h = (int)(unit_id % a.H);
+  b = (int)(unit_id / a.H);
+  return true;
+}
 
 // VG: per-key gates (GLA), staged on chip like the keys.
 template <int DK, typename T, bool CHAIN, bool VG>
@@ -41,32 +76,20 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   const int lane = threadIdx.x;
   const int c = lane & (kCols - 1);
   const int g = lane / kCols;
-  const int H = a.H, dv = a.dv, n = a.n;
-  const int ntiles = dv / kCols;
-  // neighbouring tiles (2m, 2m + 1) hold the two halves of each 128-byte row
-  // segment: their workgroups are numbered 8 apart, so that they run on the
-  // same XCD and share its L2 (consecutive workgroups go to different XCDs,
-  // whose L2s would each fetch and write back the whole lines)
-  const int npairs = (ntiles + 1) / 2;
-  const int x = blockIdx.x;
-  const int qd = x / kXcds;
-  const size_t pair = (size_t)(qd / 2) * kXcds + x % kXcds;
-  const int tile = 2 * (int)(pair % npairs) + qd % 2;
-  const size_t unit_id = pair / npairs;
-  if (tile >= ntiles || unit_id >= (size_t)a.B * H) return;  // padding of the numbering: no barrier follows
-  const int h = (int)(unit_id % H);
-  const int b = (int)(unit_id / H);
+  const int n = a.n;
+  int tile, b, h;
+  if (!slice_of(a, tile, b, h)) return;  // padding of the numbering: no barrier follows
   const int col = tile * kCols + c;
   const int row0 = g * R;
-  const size_t unit = (size_t)b * H + h;
+  const size_t unit = (size_t)b * a.H + h;
   // delta-rule families correct the value against the parent state
   const bool delta = a.family == SLA_FAMILY_GDN || a.family == SLA_FAMILY_DELTANET;
 
   // The state tile: the only state read of this call.
-  float *st = a.state + unit * DK * dv + col;
+  float *st = a.state + unit * DK * a.dv + col;
   float H0[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) H0[r] = st[(size_t)(row0 + r) * dv];
+  for (int r = 0; r < R; ++r) H0[r] = st[(size_t)(row0 + r) * a.dv];
 
   // Topology table of this draft and validation of the pending path.
   NodeTopo topo;
@@ -82,102 +105,23 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
 
   // Stage this unit's draft in LDS.
   extern __shared__ __attribute__((aligned(16))) float lds[];
-  float *ks = lds;                   // [n][DK]
-  float *qs = ks + n * DK;           // [n][DK]
-  float *gs = qs + n * DK;           // [n][DK] per-key gates (VG only)
-  float *vs = gs + (VG ? n * DK : 0);  // [n][kCols]
-  float *us = vs + n * kCols;        // [n][kCols]
-  float *als = us + n * kCols;       // [n]
-  float *bes = als + n;              // [n]
-  int *ords = reinterpret_cast<int *>(bes + n);  // [n] DFS pre-order
-  int *pars = ords + n;              // [n]
-  int *kids = pars + n;              // [n]
-  uint64_t *ancs = reinterpret_cast<uint64_t *>(kids + n + (n & 1));  // [n]
-
-  const T *q = static_cast<const T *>(a.q);
-  const T *k = static_cast<const T *>(a.k);
-  const T *v = static_cast<const T *>(a.v);
-  // eight elements per lane and step (one 16-byte load of bf16, two of fp32)
-  for (int idx = lane; idx < n * (DK / 8); idx += kWave) {
-    const int j = idx / (DK / 8), i = (idx % (DK / 8)) * 8;
-    const size_t src = (((size_t)b * n + j) * H + h) * DK + i;
-    float kv[8], qv[8];
-    load_f32<8>(k + src, kv);
-    load_f32<8>(q + src, qv);
-    float4 *kd = reinterpret_cast<float4 *>(ks + j * DK + i);
-    float4 *qd = reinterpret_cast<float4 *>(qs + j * DK + i);
-    kd[0] = make_float4(kv[0], kv[1], kv[2], kv[3]);
-    kd[1] = make_float4(kv[4], kv[5], kv[6], kv[7]);
-    qd[0] = make_float4(qv[0], qv[1], qv[2], qv[3]);
-    qd[1] = make_float4(qv[4], qv[5], qv[6], qv[7]);
-    if (VG) {
-      float gv[8];
-      load_f32<8>(a.alpha + src, gv);
-      float4 *gd = reinterpret_cast<float4 *>(gs + j * DK + i);
-      gd[0] = make_float4(gv[0], gv[1], gv[2], gv[3]);
-      gd[1] = make_float4(gv[4], gv[5], gv[6], gv[7]);
-    }
-  }
-  for (int idx = lane; idx < n * kCols; idx += kWave) {
-    const int j = idx / kCols, cc = idx % kCols;
-    vs[idx] = to_f32(v[(((size_t)b * n + j) * H + h) * dv + tile * kCols + cc]);
-  }
+  const SerialStage s = carve_stage<DK, VG>(lds, n);
+  int *ords = s.ia, *pars = s.ib, *kids = s.ic;
+  stage_draft<DK, T, VG>(a, s, b, h, tile, lane, kWave, delta, tile == 0);
   if (lane < n) {
-    const size_t s = ((size_t)b * n + lane) * H + h;
-    als[lane] = (VG || a.family == SLA_FAMILY_DELTANET) ? 1.f : a.alpha[s];
-    bes[lane] = delta ? a.beta[s] : 0.f;
     ords[topo.pos] = lane;
     pars[lane] = topo.parent;
     kids[lane] = topo.n_children;
-    ancs[lane] = topo.anc;
-  }
-  // Factor records that do not depend on the V-tile: written once per unit
-  // (k, gate) and once per sequence (parent).
-  if (tile == 0) {
-    T *fk = static_cast<T *>(a.fk);
-    constexpr int E = 16 / (int)sizeof(T);  // elements per 16-byte copy
-    for (int idx = lane; idx < n * (DK / E); idx += kWave) {
-      const int j = idx / (DK / E), i = (idx % (DK / E)) * E;
-      const size_t s = (((size_t)b * n + j) * H + h) * DK + i;
-      *reinterpret_cast<uint4 *>(fk + s) = *reinterpret_cast<const uint4 *>(k + s);
-    }
-    if (VG)
-      for (int idx = lane; idx < n * (DK / 4); idx += kWave) {
-        const int j = idx / (DK / 4), i = (idx % (DK / 4)) * 4;
-        const size_t s = (((size_t)b * n + j) * H + h) * DK + i;
-        *reinterpret_cast<float4 *>(a.falpha + s) = *reinterpret_cast<const float4 *>(a.alpha + s);
-      }
-    if (lane < n) {
-      const size_t s = ((size_t)b * n + lane) * H + h;
-      if (!VG) a.falpha[s] = a.family == SLA_FAMILY_DELTANET ? 1.f : a.alpha[s];
-      if (h == 0) a.fparent[(size_t)b * n + lane] = topo.parent;
-    }
+    s.ancs[lane] = topo.anc;
   }
   __syncthreads();
 
   // Delayed state update: commit the previous round's accepted path into the
   // tile, then write the committed tile back (the only state write).
   if (a.has_pending) {
-    const T *pk = static_cast<const T *>(a.pend.k);
-    const int pn = a.pend.n;
-    for (int t = 0; t < plen; ++t) {
-      const int node = a.pend.path[(size_t)b * pn + t];
-      const size_t s = ((size_t)b * pn + node) * H + h;
-      const float u = a.pend.u[s * dv + col];
-      float kr[R], gr[R];
-      load_f32<R>(pk + s * DK + row0, kr);
-      if (VG) {
-        load_f32<R>(a.pend.alpha + s * DK + row0, gr);
-      } else {
-        const float al = a.pend.alpha[s];
+    apply_pending<DK, R, T, VG>(a, b, h, col, row0, plen, H0);
 #pragma unroll
-        for (int r = 0; r < R; ++r) gr[r] = al;
-      }
-#pragma unroll
-      for (int r = 0; r < R; ++r) H0[r] = apply_factor(H0[r], gr[r], kr[r], u);
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r) st[(size_t)(row0 + r) * dv] = H0[r];
+    for (int r = 0; r < R; ++r) st[(size_t)(row0 + r) * a.dv] = H0[r];
   }
 
   // Node loop.
@@ -192,49 +136,18 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
 #pragma unroll
       for (int r = 0; r < R; ++r) Hc[r] = H0[r];
       if (p >= 0) {
-        uint64_t m = ancs[p];
+        uint64_t m = s.ancs[p];
         while (m) {
           const int x = __builtin_ctzll(m);
           m &= m - 1;
-          const float al = als[x];
-          const float u = us[x * kCols + c];
-          const float *kx = ks + x * DK + row0;
-          const float *gx = gs + x * DK + row0;
-#pragma unroll
-          for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], VG ? gx[r] : al, kx[r], u);
+          advance<DK, R, VG>(s, Hc, x, row0, s.us[x * kCols + c]);
         }
       }
     }
-    const float *kj = ks + j * DK + row0;
-    const float *qj = qs + j * DK + row0;
-    const float *gj = gs + j * DK + row0;
-    float sk = 0.f, sq = 0.f, kq = 0.f;
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const float kr = kj[r], qr = qj[r];
-      sk = __builtin_fmaf(Hc[r], kr, sk);
-      sq = __builtin_fmaf(Hc[r], VG ? gj[r] * qr : qr, sq);
-      kq = __builtin_fmaf(kr, qr, kq);
-    }
-    sk += __shfl_xor(sk, 16);
-    sq += __shfl_xor(sq, 16);
-    kq += __shfl_xor(kq, 16);
-    sk += __shfl_xor(sk, 32);
-    sq += __shfl_xor(sq, 32);
-    kq += __shfl_xor(kq, 32);
-    const float al = als[j], be = bes[j];
-    const float u = delta ? be * (vs[j * kCols + c] - al * sk) : vs[j * kCols + c];
-    const float o = __builtin_fmaf(kq, u, al * sq);
-    if (g == 0) {
-      const size_t s = ((size_t)b * n + j) * H + h;
-      a.out[s * dv + col] = o;
-      a.fu[s * dv + col] = u;
-      us[j * kCols + c] = u;
-    }
+    const float u = node_step<DK, R, VG>(a, s, Hc, j, b, h, c, g, row0, col, delta);
     const bool internal = CHAIN ? (t + 1 < n) : (kids[j] > 0);
     if (internal) {
-#pragma unroll
-      for (int r = 0; r < R; ++r) Hc[r] = apply_factor(Hc[r], VG ? gj[r] : al, kj[r], u);
+      advance<DK, R, VG>(s, Hc, j, row0, u);
       cur = j;
     } else {
       cur = p;
@@ -242,9 +155,141 @@ __global__ __launch_bounds__(kWave) void verify_serial_kernel(VerifyArgs a) {
   }
 }
 
-size_t serial_lds_bytes(int n, int dk, bool vg) {
-  return sizeof(float) * ((size_t)(vg ? 3 : 2) * n * dk + 2 * n * kCols + 2 * n) + sizeof(int) * (3 * n + (n & 1)) +
-         sizeof(uint64_t) * n;
+// ---------------------------------------------------------------- hybrid
+constexpr int kMaxLevels = 8;  // light edges on a root path <= log2(64) = 6
+
+// LDS beyond the stage: heavy-child keys and heavy children [n], per-level
+// chain-head lists [kMaxLevels][n], per-level counts, the error code and the
+// deepest level.
+__host__ __device__ inline size_t hybrid_extra_bytes(int n) {
+  return sizeof(int) * (2 * n + kMaxLevels * n + kMaxLevels + 2);
+}
+
+template <int DK, typename T, bool VG, int W>
+__global__ __launch_bounds__(W * kWave) void verify_hybrid_kernel(VerifyArgs a) {
+  constexpr int R = DK / kGroups;
+  const int tid = threadIdx.x;
+  const int w = tid / kWave;
+  const int lane = tid % kWave;
+  const int c = lane & (kCols - 1);
+  const int g = lane / kCols;
+  const int n = a.n;
+  int tile, b, h;
+  if (!slice_of(a, tile, b, h)) return;  // the whole workgroup: no barrier follows
+  const int col = tile * kCols + c;
+  const int row0 = g * R;
+  const size_t unit = (size_t)b * a.H + h;
+  const bool delta = a.family == SLA_FAMILY_GDN || a.family == SLA_FAMILY_DELTANET;
+
+  // every wave holds the committed tile (the pending path applied below gives
+  // bitwise the same rows in each)
+  float *st = a.state + unit * DK * a.dv + col;
+  float H0[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) H0[r] = st[(size_t)(row0 + r) * a.dv];
+
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const SerialStage s = carve_stage<DK, VG>(lds, n);
+  int *hkey = s.ia;       // [n] heavy-child key: (subtree size << 7) | (127 - child)
+  int *heavy = s.ib;      // [n] heavy child, -1 for a leaf
+  int *lists = reinterpret_cast<int *>(lds + serial_stage_bytes(n, DK, VG) / 4);  // [kMaxLevels][n]
+  int *counts = lists + kMaxLevels * n;   // [kMaxLevels]
+  int *misc = counts + kMaxLevels;        // error code, deepest level
+
+  // ---- wave 0: topology, pending-path check, heavy-light decomposition
+  if (w == 0) {
+    NodeTopo topo;
+    int err = build_topology(a.parent + (size_t)b * n, n, lane, false, topo);
+    if (err == SLA_OK && a.has_pending) {
+      err = check_path(a.pend.parent + (size_t)b * a.pend.n, a.pend.n, a.pend.path + (size_t)b * a.pend.n,
+                       a.pend.len[b], lane);
+    }
+    if (tile == 0 && h == 0 && lane == 0 && a.status) a.status[b] = err;
+    if (lane == 0) misc[0] = err;
+    if (err == SLA_OK) {
+      const bool live = lane < n;
+      // subtree size: the nodes whose root path contains this one
+      int size = 0;
+      for (int i = 0; i < n; ++i) size += (int)((readlane_u64(topo.anc, i) >> lane) & 1ull);
+      if (live) hkey[lane] = 0;
+      if (live && topo.parent >= 0) atomicMax(&hkey[topo.parent], (size << 7) | (127 - lane));
+      const int key = live ? hkey[lane] : 0;  // after every atomic of this wave (LDS keeps the wave's order)
+      const int hv = key ? 127 - (key & 127) : -1;
+      const int ph = __shfl(hv, topo.parent >= 0 ? topo.parent : 0);
+      const bool head = live && (topo.parent < 0 || ph != lane);
+      const uint64_t heads = __ballot(head);
+      // level: chain starts strictly above this node's chain head
+      const int lvl = live ? __popcll(topo.anc & heads) - 1 : 0;
+      const int hd = live ? 63 - __builtin_clzll(topo.anc & heads) : -1;  // this node's chain head
+      int len = 0;  // chain length (for a head)
+      for (int i = 0; i < n; ++i) len += __builtin_amdgcn_readlane(hd, i) == lane;
+      // rank within the level: longer chains first, then smaller head index
+      int rank = 0;
+      for (int i = 0; i < n; ++i) {
+        const uint64_t hi = heads >> i;
+        if (!(hi & 1ull)) continue;  // wave-uniform
+        const int li = __builtin_amdgcn_readlane(lvl, i);
+        const int ni = __builtin_amdgcn_readlane(len, i);
+        rank += (li == lvl) && (ni > len || (ni == len && i < lane));
+      }
+      int cnt = 0;  // lane L < kMaxLevels: chains at level L
+      for (int i = 0; i < n; ++i) {
+        const int li = __builtin_amdgcn_readlane(lvl, i);
+        cnt += ((heads >> i) & 1ull) && li == lane;
+      }
+      int deepest = head ? lvl : 0;
+      for (int o = 1; o < kWave; o <<= 1) deepest = max(deepest, __shfl_xor(deepest, o));
+      if (live) {
+        heavy[lane] = hv;
+        s.ancs[lane] = topo.anc;
+      }
+      // (heavy-light: a chain start at least halves the subtree, so a 64-node
+      // draft has at most 6 levels above level 0; the tables hold 8)
+      if (head && lvl < kMaxLevels) lists[lvl * n + rank] = lane;
+      if (lane < kMaxLevels) counts[lane] = cnt;
+      if (lane == 0) misc[1] = min(deepest, kMaxLevels - 1);
+    }
+  }
+  __syncthreads();
+  if (misc[0] != SLA_OK) return;  // workgroup-uniform
+
+  // ---- every wave: stage the draft, commit the pending path into its copy of
+  //      the tile; wave 0 writes the committed tile back
+  stage_draft<DK, T, VG>(a, s, b, h, tile, tid, W * kWave, delta, tile == 0);
+  if (a.has_pending) {
+    apply_pending<DK, R, T, VG>(a, b, h, col, row0, a.pend.len[b], H0);
+    if (w == 0) {
+#pragma unroll
+      for (int r = 0; r < R; ++r) st[(size_t)(row0 + r) * a.dv] = H0[r];
+    }
+  }
+  __syncthreads();
+
+  // ---- the chains, level by level; wave w takes ranks w, w + W, ...
+  const int deepest = misc[1];
+  for (int lvl = 0; lvl <= deepest; ++lvl) {
+    const int cnt = counts[lvl];
+    for (int r = w; r < cnt; r += W) {
+      const int head = lists[lvl * n + r];
+      // boundary state: the committed tile advanced by the head's ancestors
+      float Hc[R];
+#pragma unroll
+      for (int i = 0; i < R; ++i) Hc[i] = H0[i];
+      uint64_t m = s.ancs[head] & ~(1ull << head);
+      while (m) {
+        const int x = __builtin_ctzll(m);
+        m &= m - 1;
+        advance<DK, R, VG>(s, Hc, x, row0, s.us[x * kCols + c]);
+      }
+      for (int j = head; j >= 0;) {
+        const float u = node_step<DK, R, VG>(a, s, Hc, j, b, h, c, g, row0, col, delta);
+        const int nx = heavy[j];
+        if (nx >= 0) advance<DK, R, VG>(s, Hc, j, row0, u);
+        j = nx;
+      }
+    }
+    __syncthreads();  // this level's records are in LDS for the next
+  }
 }
 
 // gfx950 gives one workgroup up to 160 KiB of LDS; above the default 64 KiB
@@ -253,30 +298,35 @@ constexpr size_t kMaxLds = 160 * 1024;
 constexpr size_t kDefaultLds = 64 * 1024;
 
 template <typename K>
-hipError_t launch_with_lds(K kernel, dim3 grid, size_t lds, hipStream_t s, const VerifyArgs &a) {
+hipError_t launch_with_lds(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const VerifyArgs &a) {
   if (lds > kMaxLds) return hipErrorInvalidConfiguration;
   if (lds > kDefaultLds) {
     const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(kernel),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL(kernel, grid, dim3(kWave), lds, s, a);
+  hipLaunchKernelGGL(kernel, grid, block, lds, s, a);
   return hipGetLastError();
+}
+
+// tile pairs numbered in groups of eight per XCD (see slice_of), padded to whole groups
+dim3 slice_grid(const VerifyArgs &a) {
+  const size_t pairs = (size_t)a.B * a.H * ((a.dv / kCols + 1) / 2);
+  return dim3((unsigned)(((pairs + kXcds - 1) / kXcds) * 2 * kXcds));
 }
 
 template <int DK, typename T>
 hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
-  // tile pairs numbered in groups of eight per XCD (see the kernel), padded to whole groups
-  const size_t pairs = (size_t)a.B * a.H * ((a.dv / kCols + 1) / 2);
-  const dim3 grid((unsigned)(((pairs + kXcds - 1) / kXcds) * 2 * kXcds));
+  const dim3 grid = slice_grid(a);
   const bool vg = a.family == SLA_FAMILY_GLA;
-  const size_t lds = serial_lds_bytes(a.n, DK, vg);
+  const size_t lds = serial_stage_bytes(a.n, DK, vg);
+  const dim3 block(kWave);
   if (vg) {
-    if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true, true>, grid, lds, s, a);
-    return launch_with_lds(verify_serial_kernel<DK, T, false, true>, grid, lds, s, a);
+    if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true, true>, grid, block, lds, s, a);
+    return launch_with_lds(verify_serial_kernel<DK, T, false, true>, grid, block, lds, s, a);
   }
-  if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true, false>, grid, lds, s, a);
-  return launch_with_lds(verify_serial_kernel<DK, T, false, false>, grid, lds, s, a);
+  if (a.chain) return launch_with_lds(verify_serial_kernel<DK, T, true, false>, grid, block, lds, s, a);
+  return launch_with_lds(verify_serial_kernel<DK, T, false, false>, grid, block, lds, s, a);
 }
 
 template <typename T>
@@ -289,10 +339,44 @@ hipError_t launch_t(const VerifyArgs &a, hipStream_t s) {
   }
 }
 
+// Waves per workgroup: four up to 16 nodes and at d_k = 256 (two copies of a
+// 256-row slice take most of a wave's registers), else eight.
+template <int DK, typename T, int W>
+hipError_t launch_hybrid_w(const VerifyArgs &a, hipStream_t s) {
+  const dim3 grid = slice_grid(a);
+  const bool vg = a.family == SLA_FAMILY_GLA;
+  const size_t lds = serial_stage_bytes(a.n, DK, vg) + hybrid_extra_bytes(a.n);
+  const dim3 block(W * kWave);
+  if (vg) return launch_with_lds(verify_hybrid_kernel<DK, T, true, W>, grid, block, lds, s, a);
+  return launch_with_lds(verify_hybrid_kernel<DK, T, false, W>, grid, block, lds, s, a);
+}
+
+template <int DK, typename T>
+hipError_t launch_hybrid_dk(const VerifyArgs &a, hipStream_t s) {
+  if constexpr (DK == 256) return launch_hybrid_w<DK, T, 4>(a, s);
+  return a.n <= 16 ? launch_hybrid_w<DK, T, 4>(a, s) : launch_hybrid_w<DK, T, 8>(a, s);
+}
+
+template <typename T>
+hipError_t launch_hybrid_t(const VerifyArgs &a, hipStream_t s) {
+  switch (a.dk) {
+    case 64: return launch_hybrid_dk<64, T>(a, s);
+    case 128: return launch_hybrid_dk<128, T>(a, s);
+    case 256: return launch_hybrid_dk<256, T>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 }  // namespace
 
 hipError_t launch_verify_serial(const VerifyArgs &a, int dtype, hipStream_t s) {
   return dtype == SLA_DTYPE_BF16 ? launch_t<bf16>(a, s) : launch_t<float>(a, s);
+}
+
+hipError_t launch_verify_hybrid(const VerifyArgs &a, int dtype, hipStream_t s) {
+  // a chain is one chain: the serial kernel is the hybrid schedule of it
+  if (a.chain) return launch_verify_serial(a, dtype, s);
+  return dtype == SLA_DTYPE_BF16 ? launch_hybrid_t<bf16>(a, s) : launch_hybrid_t<float>(a, s);
 }
 
 }  // namespace sla

@@ -113,6 +113,9 @@ CASES = [(name, fam, route)
 # the largest GLA draft at d_k = 256 exceeds the parallel route's on-chip stage:
 # the automatic route falls back to the serial one
 CASES += [(GLA_DK256_N50.name, "gla", "serial"), (GLA_DK256_N50.name, "gla", "auto")]
+# the chain-decomposed hybrid on the tree workloads (chains run as serial)
+CASES += [(name, fam, "hybrid") for name in ["tree32_bf16", "batched_tree_serving", "large_batch_tree64"]
+          for fam in ["deltanet", "decay", "gla"]] + [(GLA_DK256_N50.name, "gla", "hybrid")]
 
 
 @pytest.mark.parametrize("name,fam,route", CASES)

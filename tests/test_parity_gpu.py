@@ -17,7 +17,7 @@ from gpu_util import (TOL, Layer, act_tensor, new_factors, new_out, oracle_commi
 
 pytestmark = pytest.mark.gpu
 
-ROUTES = ["serial", "parallel"]
+ROUTES = ["serial", "parallel", "hybrid"]
 
 
 def say(*a):

@@ -54,7 +54,7 @@ def _draft(cfg, r, kind):
 
 
 @pytest.mark.parametrize("case", CASES, ids=["c%d_B%d_H%d_dk%d_dv%d_n%d-%d" % c[:7] for c in CASES])
-@pytest.mark.parametrize("route", ["auto", "serial"])
+@pytest.mark.parametrize("route", ["auto", "serial", "hybrid"])
 def test_sweep_two_fused_rounds(case, route):
     i, Bn, H, dk, dv, n0, n1, seed = case
     r = np.random.default_rng(seed)
