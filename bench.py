@@ -164,8 +164,9 @@ def main():
     ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
                     help="measured HBM bytes per launch from rocprofv3 counters (if present)")
     ap.add_argument("--study", default=None, choices=["tree-shapes", "fused-commit"],
-                    help="tree-shapes: root-to-leaf replay, serial and parallel verification of synthetic "
-                         "top-k trees at the paper's target shape (8 heads, d_k = d_v = 256, batch 1); "
+                    help="tree-shapes: root-to-leaf replay, serial, parallel and hybrid verification of "
+                         "synthetic top-k proposal trees at the paper's target shape (8 heads, d_k = d_v = 256, "
+                         "batch 1); "
                          "fused-commit: fused commit-and-verify vs verify plus standalone commit for accepted "
                          "lengths 1..8 at verify length 4 (the same shape)")
     ap.add_argument("--op", default="gdn", choices=["gdn", "conv", "prune", "commit"],
@@ -777,19 +778,17 @@ def run_prune(args, cfg, torch, B, inputs, dev, n_cand=64, tau=3.0):
     print(json.dumps(line), flush=True)
 
 
-# proposal shapes of the paper's tree-verification table: (top-k, configured depth, nodes)
-TREE_SHAPES = [(2, 12, 16), (2, 24, 32), (4, 4, 16), (4, 4, 32), (4, 12, 16), (4, 24, 32)]
-
-
 def study_tree_shapes(args, torch, B, inputs, dev, trees_per_shape=8, reps=20):
-    """Per proposal shape: mean latency of verifying one tree (batch 1, 8
+    """Per proposal shape of the paper's tree-verification table (top-k,
+    configured depth, nodes): mean latency of verifying one synthetic
+    proposal tree (a top-k rollout pruned to the node budget; batch 1, 8
     heads, d_k = d_v = 256, bf16 activations, fp32 state, no pending commit)
-    by root-to-leaf replay (one chain verification per root-to-leaf path,
-    launched one after another from the committed state), by the serial route
-    and by the parallel route; each timed as `reps` replays of a HIP graph
-    holding ten repetitions of one tree's launches (per-tree time = total /
-    (reps x 10), the gaps between kernels included).  Also checks that the
-    three agree."""
+    by root-to-leaf replay, the serial, parallel and hybrid routes; each
+    timed as `reps` replays of a HIP graph holding ten repetitions of one
+    tree's launches (per-tree time = total / (reps x 10), the gaps between
+    kernels included).  Also checks that the four routes agree."""
+    from paper_2607_16673_amd import study
+
     H, dk, dv = 8, 256, 256
     rng = np.random.default_rng(4242)
     rows = []
@@ -816,68 +815,42 @@ def study_tree_shapes(args, torch, B, inputs, dev, trees_per_shape=8, reps=20):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) * 1e3 / (reps * per_graph)  # us per tree
 
-    for k, depth, n in TREE_SHAPES:
-        t = {"r2l": [], "serial": [], "parallel": []}
+    for si, (k, depth, n) in enumerate(study.TREE_SHAPES):
+        t = {r: [] for r in study.ROUTES}
         worst = 0.0
-        for _ in range(trees_per_shape):
-            par = inputs.random_tree(rng, n, depth, k)
-            q = inputs.bf16_bits(rng.standard_normal((1, n, H, dk)) / np.sqrt(dk))
-            kk = inputs.bf16_bits(rng.standard_normal((1, n, H, dk)) / np.sqrt(dk))
-            v = inputs.bf16_bits(rng.standard_normal((1, n, H, dv)))
-            al = (1 / (1 + np.exp(-rng.uniform(2, 5, (1, n, H))))).astype(np.float32)
-            be = (1 / (1 + np.exp(-rng.standard_normal((1, n, H))))).astype(np.float32)
-            S = (rng.standard_normal((1, H, dk, dv)) * 0.02).astype(np.float32)
-
-            def bf(x):
-                return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
-
-            qd, kd, vd = bf(q), bf(kk), bf(v)
-            ad, bd = torch.from_numpy(al).to(dev), torch.from_numpy(be).to(dev)
-            Sd = torch.from_numpy(S).to(dev)
-            pd = torch.from_numpy(par[None]).to(dev)
-            outs = {}
-            for route in ["serial", "parallel"]:
-                o = torch.empty(1, n, H, dv, dtype=torch.float32, device=dev)
-                f = B.Factors.empty(1, n, H, dk, dv, torch.bfloat16, dev)
-                outs[route] = o
-                t[route].append(timed(lambda: B.sla_verify(Sd, qd, kd, vd, ad, bd, pd, o, f, route=route)))
-            # root-to-leaf replay: one chain per leaf, gathered rows
-            leaves = [j for j in range(n) if not (par == j).any()]
-            paths = [inputs.walk_to_root(par, j) for j in leaves]
-            chains = []
-            for pth in paths:
-                ix = torch.tensor(pth, dtype=torch.long, device=dev)
-                L = len(pth)
-                chains.append(dict(q=qd[:, ix].contiguous(), k=kd[:, ix].contiguous(), v=vd[:, ix].contiguous(),
-                                   a=ad[:, ix].contiguous(), b=bd[:, ix].contiguous(),
-                                   p=torch.arange(-1, L - 1, dtype=torch.int32, device=dev)[None],
-                                   o=torch.empty(1, L, H, dv, dtype=torch.float32, device=dev),
-                                   f=B.Factors.empty(1, L, H, dk, dv, torch.bfloat16, dev), nodes=pth))
-
-            def r2l():
-                for c in chains:
-                    B.sla_verify(Sd, c["q"], c["k"], c["v"], c["a"], c["b"], c["p"], c["o"], c["f"],
-                                 topology="chain")
-
-            t["r2l"].append(timed(r2l))
-            ref = outs["serial"].cpu().numpy()
+        shape_stats = []
+        for ti in range(trees_per_shape):
+            par = study.proposal_tree(rng, k, depth, n)
+            topo = B.sla_topology_host(par)
+            shape_stats.append((topo["max_depth"], int((par == -1).sum()), len(study.root_to_leaf_paths(par))))
+            d = study.Draft(torch, dev, par, H, dk, dv, seed=100 * si + ti)
+            for route in study.ROUTES:
+                t[route].append(timed(lambda: d.launch(route)))
+            ref = d.outputs("serial")
             scale = np.max(np.abs(ref))
-            worst = max(worst, float(np.max(np.abs(outs["parallel"].cpu().numpy() - ref)) / scale))
-            for c in chains:
-                got = c["o"].cpu().numpy()[0]
-                worst = max(worst, float(np.max(np.abs(got - ref[0, c["nodes"]])) / scale))
-        r2l = float(np.mean(t["r2l"]))
-        row = {"top_k": k, "config_depth": depth, "nodes": n, "r2l_us": round(r2l, 2),
-               "serial_x": round(r2l / float(np.mean(t["serial"])), 2),
-               "parallel_x": round(r2l / float(np.mean(t["parallel"])), 2),
-               "serial_us": round(float(np.mean(t["serial"])), 2),
-               "parallel_us": round(float(np.mean(t["parallel"])), 2),
+            for route in ["r2l", "parallel", "hybrid"]:
+                worst = max(worst, float(np.max(np.abs(d.outputs(route) - ref)) / scale))
+            del d
+        mean = {r: float(np.mean(t[r])) for r in study.ROUTES}
+        st = np.array(shape_stats)
+        row = {"top_k": k, "config_depth": depth, "nodes": n, "r2l_us": round(mean["r2l"], 2),
+               "serial_x": round(mean["r2l"] / mean["serial"], 2),
+               "parallel_x": round(mean["r2l"] / mean["parallel"], 2),
+               "hybrid_x": round(mean["r2l"] / mean["hybrid"], 2),
+               "hybrid_over_serial": round(mean["serial"] / mean["hybrid"], 2),
+               "serial_us": round(mean["serial"], 2), "parallel_us": round(mean["parallel"], 2),
+               "hybrid_us": round(mean["hybrid"], 2),
+               "mean_depth": round(float(st[:, 0].mean()), 2), "mean_roots": round(float(st[:, 1].mean()), 2),
+               "mean_root_to_leaf_paths": round(float(st[:, 2].mean()), 2),
                "max_rel_diff_between_routes": worst}
-        log("tree shape k=%d depth=%d n=%d: R2L %.1f us, serial %.2fx, parallel %.2fx (routes agree to %.1e)"
-            % (k, depth, n, r2l, row["serial_x"], row["parallel_x"], worst))
+        log("tree shape k=%d depth=%d n=%d: R2L %.1f us, serial %.2fx, parallel %.2fx, hybrid %.2fx "
+            "(routes agree to %.1e)" % (k, depth, n, mean["r2l"], row["serial_x"], row["parallel_x"],
+                                        row["hybrid_x"], worst))
         rows.append(row)
     print(json.dumps({"study": "tree-shapes", "shape": {"batch": 1, "heads": H, "d_k": dk, "d_v": dv,
                                                         "qkv_dtype": "bf16", "state_dtype": "f32"},
+                      "trees": "top-k rollouts of the configured depth pruned to the node budget",
+                      "r2l": "one serial chain verification per root-to-leaf path",
                       "trees_per_shape": trees_per_shape, "rows": rows}), flush=True)
 
 

@@ -312,9 +312,10 @@ def draw_conv_state(cfg: Config, layer: int, batch: int | None = None, channels:
 
 
 # ---------------------------------------------------------------- draft rollouts
-def rollout(rng: np.random.Generator, n_cand: int, k: int = 4, vocab: int = 32, temp: float = 2.0):
-    """(parent [n_cand] int32, logp [n_cand] fp32) of one beam top-k rollout,
-    nodes in creation (topological) order."""
+def rollout(rng: np.random.Generator, n_cand: int, k: int = 4, vocab: int = 32, temp: float = 2.0,
+            max_depth: int | None = None):
+    """(parent [<= n_cand] int32, logp fp32) of one beam top-k rollout, nodes
+    in creation (topological) order; at most max_depth levels when given."""
     parent, logp, score = [], [], []
 
     def children(of):
@@ -329,7 +330,9 @@ def rollout(rng: np.random.Generator, n_cand: int, k: int = 4, vocab: int = 32, 
 
     children(-1)
     frontier = list(range(len(parent)))
-    while len(parent) < n_cand and frontier:
+    level = 1
+    while len(parent) < n_cand and frontier and (max_depth is None or level < max_depth):
+        level += 1
         best = sorted(frontier, key=lambda v: -score[v])[:k]
         start = len(parent)
         for v in best:
