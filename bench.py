@@ -147,7 +147,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--route", default="auto", choices=["auto", "serial", "parallel"])
+    ap.add_argument("--route", default="auto", choices=["auto", "serial", "parallel", "hybrid"])
     ap.add_argument("--family", default="gdn", choices=["gdn", "deltanet", "decay", "gla"],
                     help="layer family of the recurrent core (gdn: gated delta rule, the headline; deltanet: "
                          "no decay; decay: scalar decay without the delta rule; gla: per-key gates)")

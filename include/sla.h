@@ -69,7 +69,10 @@ extern "C" {
  *   AUTO      the library chooses from the topology hint and the shape:
  *             1-node drafts (the decode step) take a streaming kernel of
  *             their own (whole-line state passes, two column sums); bf16
- *             drafts the parallel route; fp32 drafts the serial route.
+ *             drafts the parallel route; fp32 chains the serial route;
+ *             fp32 trees the hybrid route above 32 nodes or when the launch
+ *             is small (batch x heads x d_v / 16 <= 512), else the serial
+ *             route.
  *   SERIAL    state-resident serial verification (§4.1): each node reduces
  *             its parent state against k_j and q_j; chains advance the
  *             on-chip state in place, trees rebuild a branch point's state

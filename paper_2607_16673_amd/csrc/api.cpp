@@ -190,10 +190,18 @@ int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
   a.falpha = factors->alpha;
   a.fparent = factors->parent;
   a.status = status;
+  // fp32 trees on the automatic route: the chain-decomposed hybrid where its
+  // parallel chains pay (64-node trees at batch 256: 9.7 ms against 11.8 ms
+  // serial; launches of few workgroups, where latency decides), else serial
+  // (16-node trees at batch 64: 129 us serial against 228 us hybrid)
+  const bool few = (size_t)shape->batch * shape->heads * (shape->d_v / 16) <= 512;
+  const bool hybrid = route == SLA_ROUTE_HYBRID ||
+                      (route == SLA_ROUTE_AUTO && !use_parallel && !chain && shape->n_nodes > 1 &&
+                       (shape->n_nodes > 32 || few));
   hipError_t e;
   if (route == SLA_ROUTE_AUTO && shape->n_nodes == 1)  // the decode step: its own streaming kernel
     e = sla::launch_verify_decode(a, shape->qkv_dtype, stream);
-  else if (route == SLA_ROUTE_HYBRID)
+  else if (hybrid)
     e = sla::launch_verify_hybrid(a, shape->qkv_dtype, stream);
   else
     e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)

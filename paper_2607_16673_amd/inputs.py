@@ -79,6 +79,10 @@ CONFIGS = {
                "batch 256, 16 heads, dk=128, dv=256, 1-node chain (decode reference)"),
         Config("paper_fused_shape", 6, 1, 8, 256, 256, 4, True, 4, 1, BF16, 1,
                "batch 1, 8 heads, dk=dv=256, chain of 4 (fused commit-and-verify study shape)"),
+        Config("batched_tree_serving_f32", 7, 64, 16, 128, 128, 16, False, 5, 3, F32, 24,
+               "batched_tree_serving with fp32 q/k/v"),
+        Config("large_batch_tree64_f32", 8, 256, 16, 128, 256, 64, False, 8, 4, F32, 1,
+               "large_batch_tree64 with fp32 q/k/v"),
     ]
 }
 
