@@ -10,7 +10,7 @@
 // u = v; GLA: per-key gates g in b and in the pending records, alpha = 1).
 //
 // One workgroup = one (b, h) unit's 64-column slab, all d_k rows (the slabs
-// of a unit numbered back to back on one XCD), laid out as in the commit
+// of a unit numbered back to back on one XCD in full launches), laid out as in the commit
 // kernel: thread t owns float4 column group t % 16 of rows
 // t / 16 + 16 r, so every state access is whole 128-byte lines, and the
 // committed rows are written through at device scope when the launch has a
@@ -50,7 +50,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(VerifyArgs a) {
   const int nslab = (dv + kCols - 1) / kCols;
   size_t uid;
   int slab;
-  if (!xcd_unit_slab((size_t)a.B * H, nslab, uid, slab)) return;  // padding: no barrier follows
+  if (!xcd_unit_slab((size_t)a.B * H, nslab, a.xcd_group, uid, slab)) return;  // padding: no barrier follows
   const int h = (int)(uid % H);
   const int b = (int)(uid / H);
   const size_t node = (size_t)b * H + h;  // record index of the draft's only node: ((b * 1 + 0) H + h)
@@ -79,10 +79,16 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(VerifyArgs a) {
   // in-place pass over 24 rotating 64 MiB states: 5.3 -> 6.2 TB/s with the
   // stores written through)
   const rsrc_t sr = make_rsrc(st, (uint32_t)DK * dv * 4);
+  // (below one workgroup per CU the launch is latency-bound: default policy)
   float4 x[R];
+  const uint32_t vo = (uint32_t)((tid / 16) * dv + cgc) * 4;
+  if (a.write_through) {
 #pragma unroll
-  for (int r = 0; r < R; ++r)
-    x[r] = buf_load_f4<kPolicyStream>(sr, (uint32_t)((tid / 16) * dv + cgc) * 4, (uint32_t)(16 * r * dv) * 4);
+    for (int r = 0; r < R; ++r) x[r] = buf_load_f4<kPolicyStream>(sr, vo, (uint32_t)(16 * r * dv) * 4);
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) x[r] = buf_load_f4<kPolicyDefault>(sr, vo, (uint32_t)(16 * r * dv) * 4);
+  }
   const T *kg = static_cast<const T *>(a.k) + node * DK;
   const T *qg = static_cast<const T *>(a.q) + node * DK;
   float kr[R], qr[R], qgr[R];  // qgr: the query scaled by the node's per-key gates (GLA)
@@ -268,7 +274,8 @@ hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
   const size_t groups = (size_t)a.B * a.H * nslab;
   VerifyArgs b = a;
   b.write_through = groups >= (size_t)device_cus();
-  hipLaunchKernelGGL(kern, dim3((unsigned)xcd_grid((size_t)a.B * a.H, nslab)), dim3(kThreads), 0, s, b);
+  b.xcd_group = b.write_through && nslab >= kXcdGroupMin;
+  hipLaunchKernelGGL(kern, dim3((unsigned)xcd_grid((size_t)a.B * a.H, nslab, b.xcd_group)), dim3(kThreads), 0, s, b);
   return hipGetLastError();
 }
 

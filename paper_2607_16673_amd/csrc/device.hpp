@@ -123,20 +123,22 @@ __device__ __forceinline__ void load_lds4(const void *g, void *lds_wave_base) {
 // (in-place pass over 3 x 512 MiB states with d_v 256 in 64-column slabs:
 // 5.6 -> 6.1 TB/s).  With two slabs per unit (d_v 128) the plain order,
 // which puts them on neighbouring XCDs, measured faster (standalone commit
-// over 24 rotating 64 MiB states: 25.9 us against 27.4 us grouped), so the
-// grouping applies from four slabs per unit on.  The grid is
-// xcd_grid(units, nslab) workgroups; the padding workgroups get false.
+// over 24 rotating 64 MiB states: 25.9 us against 27.4 us grouped), and so
+// did launches of fewer workgroups than CUs (the batch-1 commit of 8 heads at
+// d_v 256: 12.2 us against 13.6 us grouped), so the caller groups from four
+// slabs per unit on and with at least one workgroup per CU.  The grid is
+// xcd_grid(units, nslab, group) workgroups; the padding workgroups get false.
 constexpr int kXcdCount = 8;
 constexpr int kXcdGroupMin = 4;  // slabs per unit from which they are grouped
 
-__host__ __device__ inline size_t xcd_grid(size_t units, int nslab) {
-  if (nslab < kXcdGroupMin) return units * (size_t)nslab;
+__host__ __device__ inline size_t xcd_grid(size_t units, int nslab, bool group) {
+  if (!group) return units * (size_t)nslab;
   return (units + kXcdCount - 1) / kXcdCount * kXcdCount * (size_t)nslab;
 }
 
-__device__ inline bool xcd_unit_slab(size_t units, int nslab, size_t &unit, int &slab) {
+__device__ inline bool xcd_unit_slab(size_t units, int nslab, bool group, size_t &unit, int &slab) {
   const size_t i = blockIdx.x;
-  if (nslab < kXcdGroupMin) {
+  if (!group) {
     slab = (int)(i % nslab);
     unit = i / nslab;
     return unit < units;

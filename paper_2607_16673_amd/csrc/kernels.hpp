@@ -26,6 +26,7 @@ struct VerifyArgs {
   bool late_state;  // parallel route: issue the state reads after the first barrier
   bool stagger;     // parallel route: hold the state reads back briefly (a full round of workgroups)
   bool write_through;  // 1-node kernel: committed rows written through at device scope
+  bool xcd_group;      // 1-node kernel: a unit's slabs numbered back to back on one XCD
   float *state;
   PendingArgs pend;
   const void *q, *k, *v;
@@ -43,6 +44,7 @@ struct CommitArgs {
   int32_t B, H, dk, dv, n;
   bool gate_vec;       // alpha holds dk gates per record (GLA) instead of one
   bool write_through;  // state rows written through at device scope (at least one workgroup per CU)
+  bool xcd_group;      // a unit's slabs numbered back to back on one XCD
   float *state;
   const void *k;
   const float *u;
