@@ -68,11 +68,11 @@ extern "C" {
 /* Verification route (sla_shape.route).
  *   AUTO      the library chooses from the topology hint and the shape:
  *             1-node drafts (the decode step) take a streaming kernel of
- *             their own (whole-line state passes, two column sums); bf16
- *             drafts the parallel route; fp32 chains the serial route;
- *             fp32 trees the hybrid route above 32 nodes or when the launch
- *             is small (batch x heads x d_v / 16 <= 512), else the serial
- *             route.
+ *             their own (whole-line state passes, two column sums); every
+ *             other draft the parallel route.  A draft the parallel route
+ *             cannot stage on chip (see sla_verify) takes the hybrid route
+ *             if it is a tree of more than 32 nodes or the launch is small
+ *             (batch x heads x d_v / 16 <= 512), else the serial route.
  *   SERIAL    state-resident serial verification (§4.1): each node reduces
  *             its parent state against k_j and q_j; chains advance the
  *             on-chip state in place, trees rebuild a branch point's state
@@ -80,7 +80,10 @@ extern "C" {
  *   PARALLEL  tree-masked factorised verification (§4.2): one dense
  *             contraction of all queries and keys with the committed state
  *             on the matrix cores, then a tree-masked triangular solve for
- *             the corrected values and a tree-masked readout.
+ *             the corrected values and a tree-masked readout.  bf16
+ *             activations use the bf16 matrix cores (fp32 operands split
+ *             into bf16 high and low parts); fp32 activations the fp32
+ *             matrix cores, with exact fp32 products.
  *   HYBRID    chain-decomposed verification (§4.3): the draft is split by
  *             heavy-light decomposition into node-disjoint chains, each
  *             verified by the serial per-node loop; chains whose boundary
@@ -189,11 +192,12 @@ typedef struct sla_pending {
  *   factors device factor store written for this draft (see sla_factors).
  *   status  device int32 [B] or NULL: 0, SLA_ERR_TOPOLOGY or SLA_ERR_PATH.
  * The route is shape->route (SLA_ROUTE_*; an unknown value is
- * SLA_ERR_SHAPE).  Every route stages the draft on chip.  With GLA's
- * per-key gates the parallel route holds d_k = 256 drafts of up to 32 nodes
- * (PARALLEL: SLA_ERR_UNSUPPORTED above; AUTO then takes SERIAL), and the
- * serial and hybrid routes d_k = 256 drafts of up to 50 nodes
- * (SLA_ERR_UNSUPPORTED above).  Gates (alpha, GLA's g) lie in (0, 1]; every route only
+ * SLA_ERR_SHAPE).  Every route stages the draft on chip.  At d_k = 256 the
+ * parallel route holds drafts of up to 32 nodes with GLA's per-key gates or
+ * with fp32 activations (PARALLEL: SLA_ERR_UNSUPPORTED above; AUTO then
+ * takes the hybrid or serial route, as described under SLA_ROUTE_AUTO); with
+ * GLA's per-key gates the serial and hybrid routes hold d_k = 256 drafts of
+ * up to 50 nodes (SLA_ERR_UNSUPPORTED above).  Gates (alpha, GLA's g) lie in (0, 1]; every route only
  * multiplies them (decay ratios along a root path are products of the gates
  * between the two nodes), so any gate in that range, however small, is
  * valid: strong decays underflow towards zero as they do in exact

@@ -152,9 +152,11 @@ int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
   } else if (route == SLA_ROUTE_SERIAL || route == SLA_ROUTE_HYBRID) {
     use_parallel = false;
   } else {
-    // bf16 drafts, chains included, go to the tree-masked contraction on the
-    // matrix cores (its one dense contraction streams the state better than
-    // per-node reductions do); fp32 activations stay on the serial route.
+    // drafts of either activation dtype, chains included, go to the
+    // tree-masked contraction on the matrix cores: its one dense contraction
+    // streams the state better than per-node reductions do (fp32 16-node
+    // trees at batch 64: 47.8 us against 129 us serial; 64-node trees at
+    // batch 256: 0.76 ms against 9.7 ms on the hybrid)
     use_parallel = parallel_ok;
   }
 
@@ -190,14 +192,14 @@ int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
   a.falpha = factors->alpha;
   a.fparent = factors->parent;
   a.status = status;
-  // fp32 trees on the automatic route: the chain-decomposed hybrid where its
-  // parallel chains pay (64-node trees at batch 256: 9.7 ms against 11.8 ms
-  // serial; launches of few workgroups, where latency decides), else serial
-  // (16-node trees at batch 64: 129 us serial against 228 us hybrid)
+  // trees the contraction cannot stage on chip take, on the automatic route,
+  // the chain-decomposed hybrid where its parallel chains pay (fp32 64-node
+  // trees at batch 256: 9.7 ms against 11.8 ms serial; launches of few
+  // workgroups, where latency decides), else the serial route (fp32 16-node
+  // trees at batch 64: 129 us serial against 228 us hybrid)
   const bool few = (size_t)shape->batch * shape->heads * (shape->d_v / 16) <= 512;
-  const bool hybrid = route == SLA_ROUTE_HYBRID ||
-                      (route == SLA_ROUTE_AUTO && !use_parallel && !chain && shape->n_nodes > 1 &&
-                       (shape->n_nodes > 32 || few));
+  const bool hybrid_pays = !chain && shape->n_nodes > 1 && (shape->n_nodes > 32 || few);
+  const bool hybrid = route == SLA_ROUTE_HYBRID || (route == SLA_ROUTE_AUTO && !use_parallel && hybrid_pays);
   hipError_t e;
   if (route == SLA_ROUTE_AUTO && shape->n_nodes == 1)  // the decode step: its own streaming kernel
     e = sla::launch_verify_decode(a, shape->qkv_dtype, stream);
@@ -206,11 +208,13 @@ int sla_verify(const sla_shape *shape, float *state, const sla_pending *pending,
   else
     e = use_parallel ? sla::launch_verify_parallel(a, shape->qkv_dtype, stream)
                      : sla::launch_verify_serial(a, shape->qkv_dtype, stream);
-  // a draft whose on-chip stage does not fit the contraction's LDS (GLA's
-  // per-key gates at the largest shapes) is refused before any launch; the
-  // automatic route then takes the serial one
+  // a draft whose on-chip stage does not fit the contraction's LDS (more
+  // than 32 nodes at d_k = 256 with GLA's per-key gates or fp32 activations)
+  // is refused before any launch; the automatic route then takes the hybrid
+  // or the serial one by the rule above
   if (e == hipErrorInvalidConfiguration && use_parallel && route == SLA_ROUTE_AUTO)
-    e = sla::launch_verify_serial(a, shape->qkv_dtype, stream);
+    e = hybrid_pays ? sla::launch_verify_hybrid(a, shape->qkv_dtype, stream)
+                    : sla::launch_verify_serial(a, shape->qkv_dtype, stream);
   if (e == hipErrorInvalidConfiguration) return SLA_ERR_UNSUPPORTED;
   return hip_status(e);
 }

@@ -53,6 +53,8 @@
 // bf16 products) run on the column waves; they and T are done while the
 // first tile's state is still in flight.  Strided global accesses go through
 // buffer descriptors (one VGPR offset per lane).
+#include <type_traits>
+
 #include "device.hpp"
 #include "kernels.hpp"
 
@@ -82,10 +84,15 @@ constexpr int kZ = 8;                             // root paths up to this depth
 //               into bf16 hi + lo).
 constexpr int kKindDelta = 0, kKindGates = 1;
 
-template <int DK, int NP, int CW, int TPW, int KIND>
+// F32: fp32 activations.  q, k, v and the pending keys are staged and read
+// as fp32, and every contraction runs on v_mfma_f32_16x16x4_f32 with exact
+// fp32 products (no hi/lo splits); else bf16 activations (16x16x32 bf16 for
+// the Grams and P, hi/lo-split 16x16x16 bf16 for T R and Attn U).
+template <int DK, int NP, int CW, int TPW, int KIND, bool F32>
 struct Layout {
   static constexpr int kTileCols = CW * kWaveCols;
-  static constexpr int NT = NP / 16, KS = DK / 32, CH = DK / 8, MT = 2 * NT;
+  static constexpr int ES = F32 ? 4 : 2;            // bytes per activation
+  static constexpr int NT = NP / 16, KS = DK / 32, CH = DK * ES / 16, MT = 2 * NT;
   static constexpr int NB = NT * (NT + 1) / 2;      // lower-triangular 16x16 blocks
   static constexpr int kList = NP * (NP + 1) / 2;   // compact Lk capacity (floats)
   static constexpr bool kDelta = KIND == kKindDelta, kGates = KIND == kKindGates;
@@ -94,9 +101,9 @@ struct Layout {
   static constexpr int kT = kDelta ? NB * kBlk : 0;   // T blocks
   static constexpr int kAt = NB * kBlk;             // Attn blocks
   static constexpr int kLk = kDelta ? kList * 4 : 0;
-  static constexpr int kPk = kPMax * DK * 2;        // pending keys (bf16)
+  static constexpr int kPk = kPMax * DK * ES;       // pending keys (activation dtype)
   static constexpr int kPu = TPW * kPMax * kTileCols * 4;  // pending corrected values, one stage per tile
-  static constexpr int kXL = kGates ? kX / 2 : 0;   // low halves of Q~, same chunk layout
+  static constexpr int kXL = (kGates && !F32) ? kX / 2 : 0;  // low halves of Q~, same chunk layout
   static constexpr int kG = kGates ? NP * DK * 4 : 0;      // the draft's per-key gates
   static constexpr int kPg = kGates ? kPMax * DK * 4 : 0;  // pending per-key gates
   // small trees, two 64-column tiles: the second tile's first DK/2 state rows
@@ -164,8 +171,8 @@ __device__ __forceinline__ f32x4 mfma16_split(s16x4 ah, s16x4 al, s16x4 bh, s16x
 // tile state, accumulators and LDS allow a fourth resident workgroup per CU;
 // 4 (128 VGPRs) for the eight-wave form, so that two workgroups fit a CU;
 // else whatever the allocation needs.
-template <int DK, int NP, int CW>
-constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : (CW == 8 ? 4 : 1);
+template <int DK, int NP, int CW, bool F32>
+constexpr int kMinWaves = F32 ? 1 : ((DK <= 128 && NP <= 16) ? 6 : (CW == 8 ? 4 : 1));
 
 // KIND: the family's form (see Layout).  Without the delta rule Lk = 0, so
 // T = I and U = R = V: no P_k, no Lk, no T.  WT: committed rows written
@@ -177,10 +184,13 @@ constexpr int kMinWaves = (DK <= 128 && NP <= 16) ? 6 : (CW == 8 ? 4 : 1);
 template <int CW>
 constexpr int kWaves = CW == 8 ? CW : CW + 1;
 
-template <int DK, int NP, int CW, int TPW, int KIND, bool WT>
-__global__ __launch_bounds__(kWaves<CW> * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, CW>)))
+template <int DK, int NP, int CW, int TPW, int KIND, bool F32, bool WT>
+__global__ __launch_bounds__(kWaves<CW> * kWave) __attribute__((amdgpu_waves_per_eu(kMinWaves<DK, NP, CW, F32>)))
 void verify_tile_kernel(VerifyArgs a) {
-  using L = Layout<DK, NP, CW, TPW, KIND>;
+  using L = Layout<DK, NP, CW, TPW, KIND, F32>;
+  using AT = std::conditional_t<F32, float, bf16>;  // activation element
+  constexpr int ES = L::ES;
+  constexpr int EC = 16 / ES;  // activations per 16-byte chunk
   constexpr bool DELTA = KIND == kKindDelta;
   constexpr bool GV = KIND == kKindGates;
   const bool nodelta = !DELTA || a.family == SLA_FAMILY_DECAY;  // R = V
@@ -196,7 +206,7 @@ void verify_tile_kernel(VerifyArgs a) {
   float *tb = reinterpret_cast<float *>(lds + L::oT);         // T blocks
   float *ab = reinterpret_cast<float *>(lds + L::oAt);        // Attn blocks
   float *lk = reinterpret_cast<float *>(lds + L::oLk);        // compact Lk
-  bf16 *s_pk = reinterpret_cast<bf16 *>(lds + L::oPk);        // [kPMax][DK]
+  AT *s_pk = reinterpret_cast<AT *>(lds + L::oPk);            // [kPMax][DK]
   float *s_pu = reinterpret_cast<float *>(lds + L::oPu);      // [kPMax][64]
   uint4 *xl = reinterpret_cast<uint4 *>(lds + L::oXL);        // GLA: low halves of Q~
   float *s_g = reinterpret_cast<float *>(lds + L::oG);        // GLA: [NP][DK] gates
@@ -231,8 +241,8 @@ void verify_tile_kernel(VerifyArgs a) {
   const size_t nbase = (size_t)b * n;
   const rsrc_t sr = make_rsrc(a.state + unit * DK * dv, (uint32_t)DK * dv * 4);
   const uint32_t nstride = (uint32_t)H * dv;  // elements between consecutive nodes of a unit
-  const rsrc_t vr = make_rsrc(static_cast<const bf16 *>(a.v) + (nbase * H + h) * dv,
-                              ((uint32_t)(n - 1) * nstride + dv) * 2);
+  const rsrc_t vr = make_rsrc(static_cast<const AT *>(a.v) + (nbase * H + h) * dv,
+                              ((uint32_t)(n - 1) * nstride + dv) * ES);
   // wave-uniform: this wave owns columns of tile t
   auto live = [&](int t) { return w < kColWaves && t * kTileCols + w * kWaveCols < dv; };
   // state rows 8 lg + e + 32 ks of column t * kTileCols + ucol, in B-fragment order
@@ -246,17 +256,32 @@ void verify_tile_kernel(VerifyArgs a) {
   // values of node j = 16 mt + 4 lg + q; rows past the last node fall
   // outside the descriptor and read zero
   auto load_values = [&](int t, uint32_t (&vraw)[NT][4]) {
-    const uint32_t vv = (4 * lg * nstride + t * kTileCols + ucol) * 2;
+    const uint32_t vv = (4 * lg * nstride + t * kTileCols + ucol) * ES;
 #pragma unroll
     for (int mt = 0; mt < NT; ++mt)
 #pragma unroll
-      for (int q = 0; q < 4; ++q)
-        vraw[mt][q] = __builtin_amdgcn_raw_buffer_load_b16(vr, vv + (uint32_t)(mt * 16 + q) * nstride * 2, 0, kPolicyDefault);
+      for (int q = 0; q < 4; ++q) {
+        const uint32_t o = vv + (uint32_t)(mt * 16 + q) * nstride * ES;
+        if constexpr (F32)
+          vraw[mt][q] = __builtin_amdgcn_raw_buffer_load_b32(vr, o, 0, kPolicyDefault);
+        else
+          vraw[mt][q] = __builtin_amdgcn_raw_buffer_load_b16(vr, o, 0, kPolicyDefault);
+      }
+  };
+
+  // fp32 activations: the eight values k = 32 ks + 8 lg + e (e = 0..7) of
+  // stage row `row`, the A operand of v_mfma_f32_16x16x4_f32 number e of
+  // K-step ks, whose K index lg then pairs with state row 32 ks + 8 lg + e
+  // (exactly what a column wave's state registers hold as B operands)
+  auto frag8 = [&](int row, int ks, float (&x)[8]) {
+    const float4 u0 = *reinterpret_cast<const float4 *>(xs + xchunk<CH>(row, 8 * ks + 2 * lg));
+    const float4 u1 = *reinterpret_cast<const float4 *>(xs + xchunk<CH>(row, 8 * ks + 2 * lg + 1));
+    x[0] = u0.x, x[1] = u0.y, x[2] = u0.z, x[3] = u0.w, x[4] = u1.x, x[5] = u1.y, x[6] = u1.z, x[7] = u1.w;
   };
 
   // ---- column waves: the first tile's state and values, issued first
   float hfa[KS][8], hfb[KS][8];  // hfb: the next tile's state (prefetching form only)
-  uint32_t vraw[NT][4];  // bf16 bit patterns, widened where they are used
+  uint32_t vraw[NT][4];  // activation bit patterns, widened where they are used
   if (live(t0)) {
     // a full round of workgroups: hold the state reads back about two
     // microseconds (80 x 64 cycles), so that every workgroup's setup reads
@@ -275,8 +300,8 @@ void verify_tile_kernel(VerifyArgs a) {
   int maxd = 0;    // setup wave: the deepest root path (wave-uniform)
   if (w == kSetup) {
     for (int c = l; c < (L::kT + L::kAt) / 16; c += kWave) reinterpret_cast<uint4 *>(tb)[c] = make_uint4(0, 0, 0, 0);
-    const bf16 *qg = static_cast<const bf16 *>(a.q);
-    const bf16 *kg = static_cast<const bf16 *>(a.k);
+    const AT *qg = static_cast<const AT *>(a.q);
+    const AT *kg = static_cast<const AT *>(a.k);
     const bool live = l < n;
     const size_t s = (nbase + (live ? l : 0)) * H + h;
     p = live ? a.parent[nbase + l] : -1;
@@ -302,7 +327,7 @@ void verify_tile_kernel(VerifyArgs a) {
       const int P = i * kWave + l;
       const int row = P / CH, c = (P % CH) ^ (row & 7);
       const int j = row % NP;
-      load_lds16((row < NP ? qg : kg) + ((nbase + (j < n ? j : 0)) * H + h) * DK + c * 8, xs + i * kWave);
+      load_lds16((row < NP ? qg : kg) + ((nbase + (j < n ? j : 0)) * H + h) * DK + c * EC, xs + i * kWave);
     }
     if constexpr (GV) {  // the draft's per-key gates, rows 0..NP-1 (padding rows repeat node 0)
       constexpr int GC = DK / 4;  // 16-byte chunks per gate row
@@ -406,7 +431,7 @@ void verify_tile_kernel(VerifyArgs a) {
     }
   };
   if (w == kSetup && a.has_pending) {
-    const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
+    const AT *pkg = static_cast<const AT *>(a.pend.k);
     constexpr int KI = kPMax * CH / kWave;
     constexpr int GC = DK / 4;                             // 16-byte chunks per gate row
     constexpr int GI = GV ? kPMax * GC / kWave : 0;
@@ -418,7 +443,7 @@ void verify_tile_kernel(VerifyArgs a) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int i = 0; i < KI; ++i)
-      load_lds16(pkg + ((prow + nt[i]) * H + h) * DK + ((i * kWave + l) % CH) * 8, s_pk + i * kWave * 8);
+      load_lds16(pkg + ((prow + nt[i]) * H + h) * DK + ((i * kWave + l) % CH) * EC, s_pk + i * kWave * EC);
 #pragma unroll
     for (int i = 0; i < GI; ++i)
       load_lds16(a.pend.alpha + ((prow + ng[i]) * H + h) * DK + ((i * kWave + l) % GC) * 4, s_pg + i * kWave * 4);
@@ -462,8 +487,19 @@ void verify_tile_kernel(VerifyArgs a) {
       unsigned char *xb = reinterpret_cast<unsigned char *>(xs);
       unsigned char *xlb = reinterpret_cast<unsigned char *>(xl);
       // byte offset of the 4 (E = 4) or 8 key dimensions d0 .. of stage row r
-      auto xoff = [&](int r, int d0) { return xchunk<CH>(r, d0 >> 3) * 16 + ((d0 >> 2) & 1) * 8; };
+      auto xoff = [&](int r, int d0) {
+        if constexpr (F32) return xchunk<CH>(r, d0 >> 2) * 16;  // four fp32 per chunk; d0 % 4 == 0
+        return xchunk<CH>(r, d0 >> 3) * 16 + ((d0 >> 2) & 1) * 8;
+      };
       auto load_row = [&](int r, int d0, float (&x)[E]) {
+        if constexpr (F32) {
+#pragma unroll
+          for (int c = 0; c < E; c += 4) {
+            const float4 u = *reinterpret_cast<const float4 *>(xb + xoff(r, d0 + c));
+            x[c] = u.x, x[c + 1] = u.y, x[c + 2] = u.z, x[c + 3] = u.w;
+          }
+          return;
+        }
 #pragma unroll
         for (int c = 0; c < E; c += 8 < E ? 8 : E) {
           uint32_t wv[4];
@@ -521,8 +557,23 @@ void verify_tile_kernel(VerifyArgs a) {
           }
         }
         if (j >= n) {  // padding rows: zero low halves (their products are dropped)
+          if constexpr (!F32) {
 #pragma unroll
-          for (int c = 0; c < E; c += 4) *reinterpret_cast<uint2 *>(xlb + xoff(j, d0 + c)) = make_uint2(0, 0);
+            for (int c = 0; c < E; c += 4) *reinterpret_cast<uint2 *>(xlb + xoff(j, d0 + c)) = make_uint2(0, 0);
+          }
+          continue;
+        }
+        if constexpr (F32) {  // Q~ in fp32 in place of q_j; the records: the key as given, the gates
+#pragma unroll
+          for (int c = 0; c < E; c += 4) {
+            *reinterpret_cast<float4 *>(xb + xoff(j, d0 + c)) = make_float4(qc[c], qc[c + 1], qc[c + 2], qc[c + 3]);
+            if (t0 == 0) {
+              const size_t r = ((nbase + j) * H + h) * DK + d0 + c;
+              *reinterpret_cast<float4 *>(static_cast<float *>(a.fk) + r) =
+                  *reinterpret_cast<const float4 *>(xb + xoff(NP + j, d0 + c));
+              *reinterpret_cast<float4 *>(a.falpha + r) = *reinterpret_cast<const float4 *>(s_g + j * DK + d0 + c);
+            }
+          }
           continue;
         }
 #pragma unroll
@@ -574,9 +625,17 @@ void verify_tile_kernel(VerifyArgs a) {
         f32x4 g = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mr * 16 + lc, ks * 4 + lg));
-          const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
-          g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, g, 0, 0, 0);
+          if constexpr (F32) {
+            float av[8], bv[8];
+            frag8(mr * 16 + lc, ks, av);
+            frag8(NP + na * 16 + lc, ks, bv);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) g = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], bv[e], g, 0, 0, 0);
+          } else {
+            const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mr * 16 + lc, ks * 4 + lg));
+            const bf16x8 bf = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(NP + na * 16 + lc, ks * 4 + lg));
+            g = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bf, g, 0, 0, 0);
+          }
         }
         gacc[tc / kColWaves] = g;
       }
@@ -703,7 +762,7 @@ void verify_tile_kernel(VerifyArgs a) {
     f32x4 rreg[NT];
     if (cols_live) {
       const int ps = plen < kPMax ? plen : kPMax;
-      const bf16 *pkg = static_cast<const bf16 *>(a.pend.k);
+      const AT *pkg = static_cast<const AT *>(a.pend.k);
       const int pn = a.has_pending ? a.pend.n : 1;
       if (a.has_pending) {
         // the whole tile has normally landed by now: step-major, one LDS
@@ -714,10 +773,21 @@ void verify_tile_kernel(VerifyArgs a) {
           constexpr int KC = KS < 2 ? KS : 2;  // K-steps per LDS round trip
 #pragma unroll
           for (int k0 = 0; k0 < KS; k0 += KC) {
-            bf16x8 kv[KC];
-            float gv[KC][8];  // GLA: the gates of rows 32 (k0 + c) + 8 lg + e
+            float kv[KC][8];  // the key's rows 32 (k0 + c) + 8 lg + e
+            float gv[KC][8];  // GLA: the gates of the same rows
 #pragma unroll
-            for (int c = 0; c < KC; ++c) kv[c] = *reinterpret_cast<const bf16x8 *>(s_pk + st * DK + (k0 + c) * 32 + 8 * lg);
+            for (int c = 0; c < KC; ++c) {
+              if constexpr (F32) {
+                const float4 k0v = *reinterpret_cast<const float4 *>(s_pk + st * DK + (k0 + c) * 32 + 8 * lg);
+                const float4 k1v = *reinterpret_cast<const float4 *>(s_pk + st * DK + (k0 + c) * 32 + 8 * lg + 4);
+                kv[c][0] = k0v.x, kv[c][1] = k0v.y, kv[c][2] = k0v.z, kv[c][3] = k0v.w;
+                kv[c][4] = k1v.x, kv[c][5] = k1v.y, kv[c][6] = k1v.z, kv[c][7] = k1v.w;
+              } else {
+                const bf16x8 kb = *reinterpret_cast<const bf16x8 *>(s_pk + st * DK + (k0 + c) * 32 + 8 * lg);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) kv[c][e] = static_cast<float>(kb[e]);
+              }
+            }
             if constexpr (GV) {
 #pragma unroll
               for (int c = 0; c < KC; ++c) {
@@ -731,7 +801,7 @@ void verify_tile_kernel(VerifyArgs a) {
             for (int c = 0; c < KC; ++c)
 #pragma unroll
               for (int e = 0; e < 8; ++e)
-                hf[k0 + c][e] = apply_factor(hf[k0 + c][e], GV ? gv[c][e] : al, static_cast<float>(kv[c][e]), uv);
+                hf[k0 + c][e] = apply_factor(hf[k0 + c][e], GV ? gv[c][e] : al, kv[c][e], uv);
           }
         }
         // paths longer than the LDS stage read their records directly
@@ -772,7 +842,17 @@ void verify_tile_kernel(VerifyArgs a) {
       f32x4 pk[NT];
 #pragma unroll
       for (int mt = 0; mt < NT; ++mt) pk[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if constexpr (DELTA) {
+      if constexpr (DELTA && F32) {  // exact fp32 products: the state registers are the B operands
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int mt = 0; mt < NT; ++mt) {
+            float av[8];
+            frag8(NP + mt * 16 + lc, ks, av);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pk[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], hf[ks][e], pk[mt], 0, 0, 0);
+          }
+      } else if constexpr (DELTA) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           bf16x8 bhi, blo;
@@ -796,10 +876,21 @@ void verify_tile_kernel(VerifyArgs a) {
           const int j = mt * 16 + rb + q;
           uint32_t vb = vraw[mt][q];
           __asm__("" : "+v"(vb));  // keeps the widening here, not next to the load
-          const float vf = __uint_as_float(vb << 16);
+          const float vf = __uint_as_float(F32 ? vb : vb << 16);
           const float rd = DELTA ? s_be[j] * (vf - s_gamma[j] * pk[mt][q]) : vf;
           rreg[mt][q] = j < n ? (nodelta ? vf : rd) : 0.f;
         }
+      if constexpr (F32) {  // Q (GLA: Q~) H0, exact fp32 products
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int mt = 0; mt < NT; ++mt) {
+            float av[8];
+            frag8(mt * 16 + lc, ks, av);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pq[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], hf[ks][e], pq[mt], 0, 0, 0);
+          }
+      } else
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         bf16x8 bhi, blo;
@@ -841,10 +932,10 @@ void verify_tile_kernel(VerifyArgs a) {
     // products (off the path to the barrier above)
     if (w == kSetup && i == 0 && t0 == 0) {
       if constexpr (!GV) {  // GLA's key and gate records went out with Q~
-        bf16 *fk = static_cast<bf16 *>(a.fk);
+        AT *fk = static_cast<AT *>(a.fk);
         for (int c = l; c < n * CH; c += kWave) {
           const int j = c / CH, part = c % CH;
-          *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * 8) = xs[xchunk<CH>(NP + j, part)];
+          *reinterpret_cast<uint4 *>(fk + ((nbase + j) * H + h) * DK + part * EC) = xs[xchunk<CH>(NP + j, part)];
         }
       }
       if (l < n) {
@@ -856,7 +947,19 @@ void verify_tile_kernel(VerifyArgs a) {
       // ---- U = T R, then O = Gamma P_q + Attn U, on the matrix cores; A
       //      fragments are rows j = 16 mt + lc, columns 16 ks + 4 lg .. + 3
       f32x4 uacc[NT];  // same layout as R
-      if constexpr (DELTA) {
+      if constexpr (DELTA && F32) {
+        // A operand i: T[16 mt + lc][16 ks + 4 lg + i], B operand i: R[16 ks + 4 lg + i][lc]
+#pragma unroll
+        for (int mt = 0; mt < NT; ++mt) {
+          uacc[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks <= mt; ++ks) {
+            const f32x4 tv = *reinterpret_cast<const f32x4 *>(tb + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) uacc[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(tv[i], rreg[ks][i], uacc[mt], 0, 0, 0);
+          }
+        }
+      } else if constexpr (DELTA) {
         s16x4 rhi[NT], rlo[NT];
 #pragma unroll
         for (int mt = 0; mt < NT; ++mt) split4(rreg[mt], rhi[mt], rlo[mt]);
@@ -876,8 +979,10 @@ void verify_tile_kernel(VerifyArgs a) {
         for (int mt = 0; mt < NT; ++mt) uacc[mt] = rreg[mt];
       }
       s16x4 uhi[NT], ulo[NT];
+      if constexpr (!F32) {
 #pragma unroll
-      for (int mt = 0; mt < NT; ++mt) split4(uacc[mt], uhi[mt], ulo[mt]);
+        for (int mt = 0; mt < NT; ++mt) split4(uacc[mt], uhi[mt], ulo[mt]);
+      }
       // outputs and corrected values of node j at ((b n + j) H + h) dv + col;
       // rows past the last node fall outside the descriptors (the whole offset
       // is carried per lane, where the range check applies) and are dropped
@@ -888,9 +993,14 @@ void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
         for (int ks = 0; ks <= mt; ++ks) {
           const f32x4 av = *reinterpret_cast<const f32x4 *>(ab + ((mt * (mt + 1)) / 2 + ks) * (16 * kBP) + lc * kBP + 4 * lg);
-          s16x4 ah, alo;
-          split4(av, ah, alo);
-          oacc = mfma16_split(ah, alo, uhi[ks], ulo[ks], oacc);
+          if constexpr (F32) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) oacc = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i], uacc[ks][i], oacc, 0, 0, 0);
+          } else {
+            s16x4 ah, alo;
+            split4(av, ah, alo);
+            oacc = mfma16_split(ah, alo, uhi[ks], ulo[ks], oacc);
+          }
         }
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
@@ -930,13 +1040,13 @@ int device_cus() {
 // hold them back briefly instead (stagger).
 constexpr int kLateRounds = 4;
 
-template <int DK, int NP, int CW, int TPW, int KIND>
+template <int DK, int NP, int CW, int TPW, int KIND, bool F32>
 hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
-  using L = Layout<DK, NP, CW, TPW, KIND>;
+  using L = Layout<DK, NP, CW, TPW, KIND, F32>;
   const size_t lds = L::kBytes;
   if (lds > kMaxLds) return hipErrorInvalidConfiguration;
-  auto kern_wb = verify_tile_kernel<DK, NP, CW, TPW, KIND, false>;  // committed rows written back
-  auto kern_wt = verify_tile_kernel<DK, NP, CW, TPW, KIND, true>;   // written through
+  auto kern_wb = verify_tile_kernel<DK, NP, CW, TPW, KIND, F32, false>;  // committed rows written back
+  auto kern_wt = verify_tile_kernel<DK, NP, CW, TPW, KIND, F32, true>;   // written through
   if (lds > kDefaultLds) {
     for (auto k : {kern_wb, kern_wt}) {
       const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
@@ -963,13 +1073,13 @@ hipError_t launch_np_fam(const VerifyArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int DK, int NP, int CW, int TPW>
+template <int DK, int NP, int CW, int TPW, bool F32>
 hipError_t launch_np(const VerifyArgs &a, hipStream_t s) {
-  if (a.family == SLA_FAMILY_GLA) return launch_np_fam<DK, NP, CW, TPW, kKindGates>(a, s);
-  return launch_np_fam<DK, NP, CW, TPW, kKindDelta>(a, s);
+  if (a.family == SLA_FAMILY_GLA) return launch_np_fam<DK, NP, CW, TPW, kKindGates, F32>(a, s);
+  return launch_np_fam<DK, NP, CW, TPW, kKindDelta, F32>(a, s);
 }
 
-template <int DK>
+template <int DK, bool F32>
 hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
   // small trees: two V-tiles of a unit per workgroup once single tiles would
   // fill every CU's four workgroup slots twice over.  The launch is then one
@@ -979,37 +1089,46 @@ hipError_t launch_dk(const VerifyArgs &a, hipStream_t s) {
   if constexpr (DK <= 128) {
     const int ntiles = (a.dv + kWaveCols * 4 - 1) / (kWaveCols * 4);
     if (a.n <= 32 && ntiles % 2 == 0 && (size_t)a.B * a.H * ntiles >= (size_t)8 * device_cus())
-      return a.n <= 16 ? launch_np<DK, 16, 4, 2>(a, s) : launch_np<DK, 32, 4, 2>(a, s);
+      return a.n <= 16 ? launch_np<DK, 16, 4, 2, F32>(a, s) : launch_np<DK, 32, 4, 2, F32>(a, s);
   }
-  if (a.n <= 16) return launch_np<DK, 16, 4, 1>(a, s);
-  if (a.n <= 32) return launch_np<DK, 32, 4, 1>(a, s);
+  if (a.n <= 16) return launch_np<DK, 16, 4, 1, F32>(a, s);
+  if (a.n <= 32) return launch_np<DK, 32, 4, 1, F32>(a, s);
   // large trees: two V-tiles per workgroup -- topology, Grams and T serve
   // both, and the second tile's state loads overlap the first tile's U, O
   // and stores; with d_v a multiple of 256, tiles of 128 columns (eight
   // column waves), so that one workgroup covers 256 columns
   if constexpr (DK <= 128) {
-    if (a.dv % 256 == 0) return launch_np<DK, 64, 8, 2>(a, s);
-    if (((a.dv + kWaveCols * 4 - 1) / (kWaveCols * 4)) % 2 == 0) return launch_np<DK, 64, 4, 2>(a, s);
+    if (a.dv % 256 == 0) return launch_np<DK, 64, 8, 2, F32>(a, s);
+    if (((a.dv + kWaveCols * 4 - 1) / (kWaveCols * 4)) % 2 == 0) return launch_np<DK, 64, 4, 2, F32>(a, s);
   }
-  return launch_np<DK, 64, 4, 1>(a, s);
+  return launch_np<DK, 64, 4, 1, F32>(a, s);
 }
 
 }  // namespace
 
 bool parallel_supported(int dk, int dv, int n, int dtype) {
-  // The hi/lo split contraction relies on q and k being exact in bf16.
-  return dtype == SLA_DTYPE_BF16 && (dk == 64 || dk == 128 || dk == 256) && dv % 16 == 0 && n >= 1 &&
-         n <= SLA_MAX_NODES;
+  // bf16 activations: bf16 matrix cores (q and k exact in bf16, the fp32
+  // operands split hi + lo); fp32 activations: fp32 matrix cores.  A draft
+  // whose stage exceeds the LDS is refused at launch
+  // (hipErrorInvalidConfiguration).
+  return (dtype == SLA_DTYPE_BF16 || dtype == SLA_DTYPE_F32) && (dk == 64 || dk == 128 || dk == 256) &&
+         dv % 16 == 0 && n >= 1 && n <= SLA_MAX_NODES;
+}
+
+template <bool F32>
+hipError_t launch_dtype(const VerifyArgs &a, hipStream_t s) {
+  switch (a.dk) {
+    case 64: return launch_dk<64, F32>(a, s);
+    case 128: return launch_dk<128, F32>(a, s);
+    case 256: return launch_dk<256, F32>(a, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_verify_parallel(const VerifyArgs &a, int dtype, hipStream_t s) {
-  if (dtype != SLA_DTYPE_BF16) return hipErrorInvalidConfiguration;
-  switch (a.dk) {
-    case 64: return launch_dk<64>(a, s);
-    case 128: return launch_dk<128>(a, s);
-    case 256: return launch_dk<256>(a, s);
-    default: return hipErrorInvalidValue;
-  }
+  if (dtype == SLA_DTYPE_BF16) return launch_dtype<false>(a, s);
+  if (dtype == SLA_DTYPE_F32) return launch_dtype<true>(a, s);
+  return hipErrorInvalidConfiguration;
 }
 
 }  // namespace sla

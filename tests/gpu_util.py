@@ -100,3 +100,24 @@ def sample_units(cfg, count, seed, batch=None):
     # always include the corners (first and last unit)
     units = {allu[0], allu[-1]} | {allu[i] for i in idx}
     return sorted(units)
+
+
+def parallel_supported(dk, dv, n, dtype):
+    """Whether an explicit PARALLEL request for a GDN draft of this shape is
+    accepted: a shape outside the route, or a draft whose on-chip stage does
+    not fit, is refused with SLA_ERR_UNSUPPORTED before any launch."""
+    try:
+        z = torch.zeros
+        dt = torch.bfloat16 if dtype == inputs.BF16 else torch.float32
+        q = z(1, n, 1, dk, dtype=dt, device="cuda")
+        v = z(1, n, 1, dv, dtype=dt, device="cuda")
+        par = torch.arange(-1, n - 1, dtype=torch.int32, device="cuda")[None]
+        B.sla_verify(z(1, 1, dk, dv, device="cuda"), q, q, v, z(1, n, 1, device="cuda"),
+                     z(1, n, 1, device="cuda"), par, z(1, n, 1, dv, device="cuda"),
+                     B.Factors.empty(1, n, 1, dk, dv, dt), route="parallel")
+        torch.cuda.synchronize()
+        return True
+    except B.SlaError as e:
+        if e.code == B.SLA_ERR_UNSUPPORTED:
+            return False
+        raise

@@ -194,9 +194,14 @@ def test_family_argument_rules_return_before_launch():
         assert call(fam, _ptr(4), None, state=mis) == B.SLA_ERR_UNSUPPORTED
     assert call("gdn", None, _ptr(5)) == B.SLA_ERR_NULL
     assert call("gdn", _ptr(4), None) == B.SLA_ERR_NULL
-    # GLA's per-key gates on the parallel route need bf16 activations
+    # the parallel route's on-chip stage: a draft that does not fit (64 nodes
+    # of fp32 keys at d_k = 256) is refused before any launch; fp32
+    # activations otherwise pass its host checks (stopped here by the
+    # misaligned state pointer)
+    big = B.make_shape(2, 4, 256, 64, 64, "f32", family="gdn")
+    assert call("gdn", _ptr(4), _ptr(5), route=B.SLA_ROUTE_PARALLEL, shape=big) == B.SLA_ERR_UNSUPPORTED
     s32 = B.make_shape(2, 4, 128, 128, 8, "f32", family="gla")
-    assert call("gla", _ptr(4), None, route=B.SLA_ROUTE_PARALLEL, shape=s32) == B.SLA_ERR_UNSUPPORTED
+    assert call("gla", _ptr(4), None, state=mis, route=B.SLA_ROUTE_PARALLEL, shape=s32) == B.SLA_ERR_UNSUPPORTED
     assert call("gla", ctypes.c_void_p(FAKE + 4 * (1 << 24) + 4), None) == B.SLA_ERR_UNSUPPORTED  # gates misaligned
     bad = B.make_shape(2, 4, 128, 128, 8, "bf16")
     bad.family = 4

@@ -12,6 +12,8 @@ import torch
 from paper_2607_16673_amd import binding as B
 from paper_2607_16673_amd import inputs
 
+from gpu_util import parallel_supported
+
 pytestmark = pytest.mark.gpu
 
 GUARD_BYTES = 1 << 16  # on each side; a multiple of 16 keeps the interior aligned
@@ -74,15 +76,17 @@ SHAPES = [  # B, H, dk, dv, n
 ]
 
 
+@pytest.mark.parametrize("dt", [inputs.BF16, inputs.F32])
 @pytest.mark.parametrize("fam", ["gdn", "gla"])
 @pytest.mark.parametrize("route", ["auto", "serial", "parallel", "hybrid"])
 @pytest.mark.parametrize("shape", SHAPES, ids=["B%d_H%d_dk%d_dv%d_n%d" % s for s in SHAPES])
-def test_verify_and_commit_stay_in_bounds(shape, route, fam):
+def test_verify_and_commit_stay_in_bounds(shape, route, fam, dt):
     Bn, H, dk, dv, n = shape
-    dt = inputs.BF16
-    tdt = torch.bfloat16
+    tdt = torch.bfloat16 if dt == inputs.BF16 else torch.float32
     if route == "parallel" and fam == "gla" and dk == 256 and n > 32:
         pytest.skip("GLA's parallel stage holds at most 32 nodes at d_k = 256")
+    if route == "parallel" and not parallel_supported(dk, dv, n, dt):
+        pytest.skip("the draft's on-chip stage does not fit the parallel route")
     cfg = inputs.Config("canary", 900 + dk + n, Bn, H, dk, dv, n, False, min(n, 6), 4, dt, 1)
     r = np.random.default_rng(Bn * 1000 + dk + n)
     G = Guarded()
@@ -112,7 +116,7 @@ def test_verify_and_commit_stay_in_bounds(shape, route, fam):
                         G.make(inputs_gate_shape(Bn, n, H, dk, fam), torch.float32), G.make((Bn, n), torch.int32))))
     state = G.make((Bn, H, dk, dv), torch.float32, torch.from_numpy(inputs.draw_state(cfg, 0)))
     status = G.make((Bn,), torch.int32)
-    say("canary verify %s route=%s fam=%s" % (shape, route, fam))
+    say("canary verify %s route=%s fam=%s dtype=%s" % (shape, route, fam, dt))
     R0, R1 = rounds
     B.sla_verify(state, R0["q"], R0["k"], R0["v"], R0["a"], R0["b"], R0["parent"], R0["out"], R0["f"],
                  status=status, route=route, family=fam)

@@ -108,8 +108,10 @@ CASES = [(name, fam, route)
          for name in ["tiny_chain_f32", "chain8_bf16", "tree32_bf16", "paper_fused_shape",
                       "batched_tree_serving", "large_batch_tree64"]
          for fam in ["deltanet", "decay", "gla"]
-         for route in ["serial", "parallel"]
-         if not (route == "parallel" and name == "tiny_chain_f32")]
+         for route in ["serial", "parallel"]]
+# fp32 q/k/v on the parallel route (the fp32 matrix-core contraction)
+CASES += [(name, fam, "parallel") for name in ["batched_tree_serving_f32", "large_batch_tree64_f32"]
+          for fam in ["deltanet", "decay", "gla"]]
 # the largest GLA draft at d_k = 256 exceeds the parallel route's on-chip stage:
 # the automatic route falls back to the serial one
 CASES += [(GLA_DK256_N50.name, "gla", "serial"), (GLA_DK256_N50.name, "gla", "auto")]

@@ -44,6 +44,9 @@ def _elementwise_ok(x, ref, tol):
     ("large_batch_tree64", [0], "auto"),
     ("large_batch_tree64", [0], "serial"),
     ("large_batch_chain1", [0], "auto"),
+    ("batched_tree_serving_f32", [0, 23], "parallel"),
+    ("large_batch_tree64_f32", [0], "parallel"),
+    ("large_batch_tree64_f32", [0], "auto"),
 ])
 def test_full_size_two_rounds(name, layers_checked, route):
     cfg = inputs.config(name)

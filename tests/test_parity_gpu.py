@@ -12,7 +12,7 @@ import oracle
 from paper_2607_16673_amd import binding as B
 from paper_2607_16673_amd import inputs
 
-from gpu_util import (TOL, Layer, act_tensor, new_factors, new_out, oracle_commit_units,
+from gpu_util import (TOL, parallel_supported, Layer, act_tensor, new_factors, new_out, oracle_commit_units,
                       oracle_verify_units, rel_err, sample_units, verify)
 
 pytestmark = pytest.mark.gpu
@@ -116,26 +116,7 @@ def test_verify_and_commit_small_configs(name, route):
 def _parallel_ok(cfg):
     # a PARALLEL request on an unsupported shape is rejected host-side, before
     # any launch, with SLA_ERR_UNSUPPORTED
-    return _parallel_supported(cfg.d_k, cfg.d_v, cfg.n_nodes, cfg.dtype)
-
-
-def _parallel_supported(dk, dv, n, dtype):
-    try:
-        cfg = inputs.Config("probe", 99, 1, 1, dk, dv, n, False, n, 64, dtype, 1)
-        z = torch.zeros
-        dt = torch.bfloat16 if dtype == inputs.BF16 else torch.float32
-        q = z(1, n, 1, dk, dtype=dt, device="cuda")
-        v = z(1, n, 1, dv, dtype=dt, device="cuda")
-        par = torch.arange(-1, n - 1, dtype=torch.int32, device="cuda")[None]
-        B.sla_verify(z(1, 1, dk, dv, device="cuda"), q, q, v, z(1, n, 1, device="cuda"),
-                     z(1, n, 1, device="cuda"), par, z(1, n, 1, dv, device="cuda"),
-                     B.Factors.empty(1, n, 1, dk, dv, dt), route="parallel")
-        torch.cuda.synchronize()
-        return True
-    except B.SlaError as e:
-        if e.code == B.SLA_ERR_UNSUPPORTED:
-            return False
-        raise
+    return parallel_supported(cfg.d_k, cfg.d_v, cfg.n_nodes, cfg.dtype)
 
 
 # ------------------------------------------- fused commit-and-verify (§5.2)
@@ -169,6 +150,14 @@ LARGE = [
     # work on wave 0; 1024 workgroups are one full round at two per CU on a
     # 256-CU part (state reads held back, committed rows written through)
     inputs.Config("tree48_dv256_round", 115, 64, 16, 128, 256, 48, False, 8, 4, inputs.BF16, 1),
+    # fp32 q/k/v on the fp32 matrix-core contraction: paired tiles with the
+    # early-staged state rows, d_k 64 and 256, eight-wave 128-column tiles,
+    # and a 64-node tree (a 64-row node block)
+    inputs.Config("pair_tree13_f32", 118, 64, 16, 128, 128, 13, False, 5, 3, inputs.F32, 1),
+    inputs.Config("pair_tree11_dk64_f32", 119, 64, 16, 64, 128, 11, False, 4, 3, inputs.F32, 1),
+    inputs.Config("tree30_dv80_dk256_f32", 120, 2, 3, 256, 80, 30, False, 10, 3, inputs.F32, 1),
+    inputs.Config("tree48_dv256_round_f32", 121, 64, 16, 128, 256, 48, False, 8, 4, inputs.F32, 1),
+    inputs.Config("tree64_dv144_f32", 122, 3, 2, 128, 144, 64, False, 12, 4, inputs.F32, 1),
 ]
 
 

@@ -8,11 +8,13 @@ nodes of a root path).
 Per case, two rounds through the C ABI: round 0 verified from the committed
 state; round 1 with round 0's accepted path pending (fused commit-and-
 verify).  Every output and committed state must be finite; sampled (b, h)
-units are compared with the fp64 oracle (bar 2e-3 normwise, bf16 q/k/v);
+units are compared with the fp64 oracle (bar 2e-3 normwise with bf16
+q/k/v, 1e-5 with fp32);
 the serial and parallel routes are compared over every unit.  The shapes:
 64-deep chains, the 64-node depth-8 trees at batch 256 (d_v 256), the
 paper's target shape (8 heads, d_k = d_v = 256) as a chain of 4 and a
-32-node tree, and the 16-node trees at batch 64."""
+32-node tree, the 16-node trees at batch 64, and with fp32 q/k/v a 32-deep
+chain and a 48-node tree."""
 import numpy as np
 import pytest
 import torch
@@ -42,7 +44,12 @@ CHAIN64 = inputs.Config("chain64_strong", 60, 4, 4, 128, 128, 64, True, 64, 1, i
                         "batch 4, 4 heads, dk=dv=128, 64-deep chain")
 PAPER_TREE32 = inputs.Config("paper_tree32_strong", 61, 1, 8, 256, 256, 32, False, 6, 4, inputs.BF16, 1,
                              "batch 1, 8 heads, dk=dv=256, 32-node tree (depth<=6, branch<=4)")
-CFGS = {c.name: c for c in [CHAIN64, PAPER_TREE32]}
+# fp32 activations (the fp32 matrix-core contraction on the parallel route)
+CHAIN32_F32 = inputs.Config("chain32_strong_f32", 62, 4, 4, 128, 128, 32, True, 32, 1, inputs.F32, 1,
+                            "batch 4, 4 heads, dk=dv=128, 32-deep chain, fp32 q/k/v")
+TREE48_F32 = inputs.Config("tree48_strong_f32", 63, 8, 4, 128, 192, 48, False, 8, 4, inputs.F32, 1,
+                           "batch 8, 4 heads, dk=128, dv=192, 48-node tree (depth<=8), fp32 q/k/v")
+CFGS = {c.name: c for c in [CHAIN64, PAPER_TREE32, CHAIN32_F32, TREE48_F32]}
 
 
 def _cfg(name):
@@ -73,7 +80,7 @@ class Draft:
 
 def _run(cfg, fam, route, S0, d0, d1):
     """Two rounds; returns (committed state, round-1 outputs) on the host."""
-    dt = torch.bfloat16
+    dt = torch.bfloat16 if cfg.dtype == inputs.BF16 else torch.float32
     Bn, n, H = cfg.batch, cfg.n_nodes, cfg.heads
     f0 = B.Factors.empty(Bn, n, H, cfg.d_k, cfg.d_v, dt, family=fam)
     f1 = B.Factors.empty(Bn, n, H, cfg.d_k, cfg.d_v, dt, family=fam)
@@ -92,7 +99,8 @@ def _run(cfg, fam, route, S0, d0, d1):
 
 
 CASES = [(name, fam) for name in ["chain64_strong", "large_batch_tree64", "paper_fused_shape",
-                                  "paper_tree32_strong", "batched_tree_serving"]
+                                  "paper_tree32_strong", "batched_tree_serving", "chain32_strong_f32",
+                                  "tree48_strong_f32"]
          for fam in ["gdn", "decay", "gla"]]
 
 

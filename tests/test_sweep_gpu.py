@@ -14,7 +14,8 @@ import oracle
 from paper_2607_16673_amd import binding as B
 from paper_2607_16673_amd import inputs
 
-from gpu_util import TOL, Layer, new_factors, new_out, oracle_commit_units, oracle_verify_units, rel_err
+from gpu_util import (TOL, Layer, new_factors, new_out, oracle_commit_units, oracle_verify_units, parallel_supported,
+                      rel_err)
 
 pytestmark = pytest.mark.gpu
 
@@ -56,11 +57,25 @@ def _draft(cfg, r, kind):
 @pytest.mark.parametrize("case", CASES, ids=["c%d_B%d_H%d_dk%d_dv%d_n%d-%d" % c[:7] for c in CASES])
 @pytest.mark.parametrize("route", ["auto", "serial", "hybrid"])
 def test_sweep_two_fused_rounds(case, route):
+    _sweep_case(case, route, inputs.BF16)
+
+
+@pytest.mark.parametrize("case", CASES, ids=["c%d_B%d_H%d_dk%d_dv%d_n%d-%d" % c[:7] for c in CASES])
+def test_sweep_two_fused_rounds_f32_parallel(case):
+    """The same cases with fp32 q/k/v on the fp32 matrix-core contraction
+    (1e-5 bar); a draft whose on-chip stage would not fit is refused."""
+    _sweep_case(case, "parallel", inputs.F32)
+
+
+def _sweep_case(case, route, dt):
     i, Bn, H, dk, dv, n0, n1, seed = case
     r = np.random.default_rng(seed)
-    say("sweep case %d route %s: B=%d H=%d dk=%d dv=%d n0=%d n1=%d" % (i, route, Bn, H, dk, dv, n0, n1))
-    c0 = inputs.Config("sw0", 300 + i, Bn, H, dk, dv, n0, False, n0, 64, inputs.BF16, 1)
-    c1 = inputs.Config("sw1", 400 + i, Bn, H, dk, dv, n1, False, n1, 64, inputs.BF16, 1)
+    say("sweep case %d route %s dtype %s: B=%d H=%d dk=%d dv=%d n0=%d n1=%d"
+        % (i, route, dt, Bn, H, dk, dv, n0, n1))
+    if route == "parallel" and not all(parallel_supported(dk, dv, m, dt) for m in (n0, n1)):
+        pytest.skip("the draft's on-chip stage does not fit the parallel route")
+    c0 = inputs.Config("sw0", 300 + i, Bn, H, dk, dv, n0, False, n0, 64, dt, 1)
+    c1 = inputs.Config("sw1", 400 + i, Bn, H, dk, dv, n1, False, n1, 64, dt, 1)
     r0 = inputs.draw_round(c0, 0, layers=[0])
     r1 = inputs.draw_round(c1, 0, layers=[0])
     r0.parent = _draft(c0, r, ["tree", "chain", "forest"][i % 3])
@@ -102,7 +117,7 @@ def test_sweep_two_fused_rounds(case, route):
     got = out1.cpu().numpy()
     eo = rel_err(np.stack([got[b, :, h] for b, h in units]), np.stack([ref[u] for u in units]))
     say("sweep case %d route %s: state err %.2e output err %.2e" % (i, route, es, eo))
-    assert es <= TOL[inputs.BF16] and eo <= TOL[inputs.BF16]
+    assert es <= TOL[dt] and eo <= TOL[dt]
 
 
 @pytest.mark.parametrize("case", CASES[:12], ids=["c%d" % c[0] for c in CASES[:12]])
