@@ -9,7 +9,10 @@ pass for FETCH_SIZE, one for WRITE_SIZE; the counters cannot share a pass):
   summarize reads the counter CSVs of the copy passes and of the bench
             passes and writes the calibrated HBM bytes per verify launch to
             profiles/traffic.json, which bench.py reports as
-            roofline.traffic.
+            roofline.traffic;
+  sizes     checks the read calibration against the L2's read requests to
+            HBM counted by size (32, 64 and 128 bytes), one more pass each
+            over the copy and the bench.
 
 Example (the full commands are recorded next to the numbers in profiles/):
 
@@ -145,6 +148,51 @@ def summarize(out_dir: str, workload: str, route: str, mode: str, skip: int, jso
     return {key: entry}
 
 
+SIZE_COUNTERS = {32: "TCC_EA0_RDREQ_32B_sum", 64: "TCC_EA0_RDREQ_64B_sum", 128: "TCC_EA0_RDREQ_128B_sum"}
+
+
+def _bytes_by_request_size(dirname: str, tag: str, skip: int):
+    """Read bytes per dispatch from the L2's read requests to HBM counted by
+    size (one pass holding the three SIZE_COUNTERS), and the request counts."""
+    counts = {}
+    n = 0
+    for size, name in SIZE_COUNTERS.items():
+        v, n = _per_dispatch_kib(_rows(dirname, name), tag, skip)
+        counts[size] = v
+    return sum(size * c for size, c in counts.items()), counts, n
+
+
+def summarize_sizes(out_dir: str, key: str, skip: int, json_path: str, kernel: str = KERNEL_TAG) -> dict:
+    """Checks the FETCH_SIZE calibration with a direct count.  The copy and
+    the bench each get one rocprofv3 --pmc pass over SIZE_COUNTERS (folders
+    copy_sizes and bench_sizes); the read bytes are 32, 64 and 128 times the
+    requests of each size.  Recorded beside the calibrated entry `key` of
+    traffic.json: the direct count per launch, the request mix, and its
+    ratio to the calibrated FETCH_SIZE figure (1.0 when the copy's scale
+    holds for this kernel) and to the copy's known bytes."""
+    copy_bytes = COPY_MIB * (1 << 20)
+    cb, ccounts, _ = _bytes_by_request_size(os.path.join(out_dir, "copy_sizes"), COPY_TAG, 0)
+    kb, kcounts, n = _bytes_by_request_size(os.path.join(out_dir, "bench_sizes"), kernel, skip)
+    with open(json_path) as f:
+        data = json.load(f)
+    if key not in data:
+        raise KeyError("no calibrated entry %r in %s" % (key, json_path))
+    entry = data[key]
+    tot = sum(kcounts.values()) or 1.0
+    entry["read_check"] = {
+        "fetch_bytes_by_request_size": int(round(kb)),
+        "request_mix": {str(s): round(c / tot, 4) for s, c in kcounts.items()},
+        "ratio_to_calibrated_fetch": round(kb / entry["fetch_bytes_per_launch"], 4),
+        "copy_bytes_by_request_size_over_known": round(cb / copy_bytes, 4),
+        "dispatches": n,
+        "source_sha256": source_digest(kernel),
+    }
+    with open(json_path, "w") as f:
+        json.dump(data, f, indent=1, sort_keys=True)
+        f.write("\n")
+    return {key: entry["read_check"]}
+
+
 MFMA_COUNTERS = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_BUSY_CU_CYCLES", "GRBM_GUI_ACTIVE"]
 
 
@@ -216,8 +264,16 @@ def main(argv=None) -> None:
     m.add_argument("--workload", required=True)
     m.add_argument("--skip", type=int, default=0)
     m.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
+    z = sub.add_parser("sizes", help="check the FETCH_SIZE calibration with read requests counted by size")
+    z.add_argument("--out-dir", required=True)
+    z.add_argument("--key", required=True, help="traffic.json entry, e.g. batched_tree_serving/auto/fused")
+    z.add_argument("--kernel", default=KERNEL_TAG)
+    z.add_argument("--skip", type=int, default=0)
+    z.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     a = ap.parse_args(argv)
-    if a.cmd == "copy":
+    if a.cmd == "sizes":
+        print(json.dumps(summarize_sizes(a.out_dir, a.key, a.skip, a.json, a.kernel), indent=1))
+    elif a.cmd == "copy":
         run_copy(a.mib)
     elif a.cmd == "mfma":
         print(json.dumps(summarize_mfma(a.out_dir, a.workload, a.skip, a.json), indent=1))
