@@ -193,15 +193,22 @@ def summarize_sizes(out_dir: str, key: str, skip: int, json_path: str, kernel: s
     return {key: entry["read_check"]}
 
 
-MFMA_COUNTERS = ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_BUSY_CU_CYCLES", "GRBM_GUI_ACTIVE"]
+def mfma_counters(dtype: str = "bf16"):
+    """The counters of one matrix-core pass: busy cycles, the MFMA operations
+    of the activation dtype's products (bf16 or f32), CU and GPU activity."""
+    return ["SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_%s" % dtype.upper(), "SQ_BUSY_CU_CYCLES",
+            "GRBM_GUI_ACTIVE"]
+
+
+MFMA_COUNTERS = mfma_counters("bf16")
 
 
 def summarize_mfma(out_dir: str, workload: str, skip: int, json_path: str, kernel: str = KERNEL_TAG,
-                   simds: int = 1024) -> dict:
+                   simds: int = 1024, dtype: str = "bf16") -> dict:
     """Matrix-core use of the verify kernel from one rocprofv3 --pmc pass with
-    MFMA_COUNTERS, per launch: MFMA busy cycles per SIMD (busy cycles summed
-    over the SIMDs / simds) and the bf16 MFMA operations
-    (SQ_INSTS_VALU_MFMA_MOPS_BF16 counts multiply and add operations / 512).
+    mfma_counters(dtype), per launch: MFMA busy cycles per SIMD (busy cycles
+    summed over the SIMDs / simds) and the MFMA operations of that dtype
+    (SQ_INSTS_VALU_MFMA_MOPS_* counts multiply and add operations / 512).
     GRBM_GUI_ACTIVE is kept for reference only: under counter collection it
     spans more than the kernel (dispatches are serialised and sampled), so
     utilisation is taken against the kernel-trace duration instead."""
@@ -225,11 +232,12 @@ def summarize_mfma(out_dir: str, workload: str, skip: int, json_path: str, kerne
     rows = [acc[d] for d in order][skip:]
     if not rows:
         raise ValueError("no dispatch of %r" % kernel)
-    mean = {c: sum(r.get(c, 0.0) for r in rows) / len(rows) for c in MFMA_COUNTERS}
+    counters = mfma_counters(dtype)
+    mean = {c: sum(r.get(c, 0.0) for r in rows) / len(rows) for c in counters}
     entry = {
         "kernel": kernel, "dispatches": len(rows), "simds": simds,
         "mfma_busy_cycles_per_simd": mean["SQ_VALU_MFMA_BUSY_CYCLES"] / simds,
-        "bf16_mfma_flops": mean["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512,
+        "%s_mfma_flops" % dtype.lower(): mean[counters[1]] * 512,
         "gui_active_cycles_under_collection": mean["GRBM_GUI_ACTIVE"],
         "source_sha256": source_digest(kernel),
     }
@@ -263,6 +271,7 @@ def main(argv=None) -> None:
     m.add_argument("--out-dir", required=True)
     m.add_argument("--workload", required=True)
     m.add_argument("--skip", type=int, default=0)
+    m.add_argument("--dtype", default="bf16", help="bf16 or f32: the MFMA operations counted")
     m.add_argument("--json", default=os.path.join(ROOT, "profiles", "traffic.json"))
     z = sub.add_parser("sizes", help="check the FETCH_SIZE calibration with read requests counted by size")
     z.add_argument("--out-dir", required=True)
@@ -276,7 +285,7 @@ def main(argv=None) -> None:
     elif a.cmd == "copy":
         run_copy(a.mib)
     elif a.cmd == "mfma":
-        print(json.dumps(summarize_mfma(a.out_dir, a.workload, a.skip, a.json), indent=1))
+        print(json.dumps(summarize_mfma(a.out_dir, a.workload, a.skip, a.json, dtype=a.dtype), indent=1))
     else:
         print(json.dumps(summarize(a.out_dir, a.workload, a.route, a.mode, a.skip, a.json, a.kernel, a.family),
                          indent=1))

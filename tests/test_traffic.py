@@ -87,3 +87,18 @@ def test_missing_kernel_is_an_error(tmp_path):
     _write(d, _rows("other_kernel", "FETCH_SIZE", [1.0]))
     with pytest.raises(ValueError):
         T._per_dispatch_kib(T._rows(d, "FETCH_SIZE"), "verify_tile_kernel")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_mfma_summary_counts_the_dtype_operations(tmp_path, dtype):
+    d = str(tmp_path / "mfma")
+    kern = "void sla::verify_tile_kernel<128, 64, 8, 2, 0, true, false>(sla::VerifyArgs)"
+    names = T.mfma_counters(dtype)
+    rows = []
+    for name, vals in zip(names, [[0, 4096.0, 4096.0], [0, 1000.0, 3000.0], [0, 7.0, 7.0], [0, 50.0, 70.0]]):
+        rows += _rows(kern, name, vals, instances=1)
+    _write(d, rows)
+    e = T.summarize_mfma(d, "w", 1, str(tmp_path / "t.json"), dtype=dtype)
+    assert e["%s_mfma_flops" % dtype] == 2000.0 * 512
+    assert e["mfma_busy_cycles_per_simd"] == 4096.0 / 1024
+    assert e["dispatches"] == 2
