@@ -4,6 +4,8 @@ paths pending, factor stores ping-ponged; the recurrent core and the short
 convolution) is replayed several times, with eager work and synchronisations
 in between, and every replay's states, outputs and factors are compared bit
 for bit with the same rounds run eagerly from the same starting states."""
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -20,17 +22,20 @@ def say(*a):
     print(*a, flush=True)
 
 
-def test_graph_replays_match_eager_rounds():
-    cfg = inputs.Config("graph", 120, 8, 4, 128, 128, 16, False, 5, 3, inputs.BF16, 1)
-    D = inputs.conv_channels(cfg)
+@pytest.mark.parametrize("dt", [inputs.BF16, inputs.F32])
+def test_graph_replays_match_eager_rounds(dt):
+    """dt: the recurrent core's q/k/v (bf16: the bf16 matrix-core contraction;
+    fp32: the fp32 one); the convolution runs on bf16 rows in both."""
+    cfg = inputs.Config("graph", 120, 8, 4, 128, 128, 16, False, 5, 3, dt, 1)
+    ccfg = dataclasses.replace(cfg, dtype=inputs.BF16)
     rnd = inputs.draw_round(cfg, 0, layers=[0])
     L = Layer(cfg, rnd, 0)
     S0 = inputs.draw_state(cfg, 0)
-    xa = [inputs.draw_conv_x(cfg, 0, r)[0] for r in range(2)]
+    xa = [inputs.draw_conv_x(ccfg, 0, r)[0] for r in range(2)]
     to_bf = lambda x: torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
     xs = [to_bf(x) for x in xa]
-    w = torch.from_numpy(inputs.draw_conv_weight(cfg, 0)).cuda()
-    C0 = torch.from_numpy(inputs.draw_conv_state(cfg, 0)).cuda()
+    w = torch.from_numpy(inputs.draw_conv_weight(ccfg, 0)).cuda()
+    C0 = torch.from_numpy(inputs.draw_conv_state(ccfg, 0)).cuda()
 
     def make():
         return dict(S=torch.from_numpy(S0).cuda(), C=C0.clone(), f=[new_factors(cfg), new_factors(cfg)],
@@ -67,4 +72,4 @@ def test_graph_replays_match_eager_rounds():
         for s in range(2):
             assert torch.equal(eager["f"][s].u, graph["f"][s].u), (rep, s)
             assert torch.equal(eager["f"][s].k, graph["f"][s].k), (rep, s)
-        say("graph replay %d matches the eager rounds" % rep)
+        say("graph replay %d matches the eager rounds (%s q/k/v)" % (rep, dt))
