@@ -37,10 +37,14 @@ def _gpu():
 
 GLA_DK256_N50 = inputs.Config("gla_dk256_n50", 50, 2, 2, 256, 64, 50, False, 7, 4, inputs.BF16, 1,
                               "batch 2, 2 heads, dk=256, dv=64, 50-node tree (the largest GLA draft at dk=256)")
+# d_k = 256 with fp32 activations: 30 nodes, inside the parallel route's
+# fp32 stage (the fp32 matrix cores; GLA's fp32 Q~)
+F32_DK256_N30 = inputs.Config("f32_dk256_n30", 52, 2, 3, 256, 80, 30, False, 7, 4, inputs.F32, 1,
+                              "batch 2, 3 heads, dk=256, dv=80, 30-node tree, fp32 q/k/v")
 
 
 def _cfg(name):
-    return GLA_DK256_N50 if name == GLA_DK256_N50.name else inputs.config(name)
+    return {c.name: c for c in (GLA_DK256_N50, F32_DK256_N30)}.get(name) or inputs.config(name)
 
 
 def _dev(x):
@@ -110,8 +114,10 @@ CASES = [(name, fam, route)
          for fam in ["deltanet", "decay", "gla"]
          for route in ["serial", "parallel"]]
 # fp32 q/k/v on the parallel route (the fp32 matrix-core contraction)
-CASES += [(name, fam, "parallel") for name in ["batched_tree_serving_f32", "large_batch_tree64_f32"]
+CASES += [(name, fam, "parallel") for name in ["batched_tree_serving_f32", "large_batch_tree64_f32",
+                                                F32_DK256_N30.name]
           for fam in ["deltanet", "decay", "gla"]]
+CASES += [(F32_DK256_N30.name, "gla", "auto")]
 # the largest GLA draft at d_k = 256 exceeds the parallel route's on-chip stage:
 # the automatic route falls back to the serial one
 CASES += [(GLA_DK256_N50.name, "gla", "serial"), (GLA_DK256_N50.name, "gla", "auto")]
@@ -240,10 +246,24 @@ def test_family_sweep_two_fused_rounds(case, route):
     16/32/64 blocks, trees and forests, pending rounds of another size):
     two fused rounds against verify + standalone commit bitwise, and the
     committed state and second outputs against the oracle."""
+    _family_sweep_case(case, route, inputs.BF16)
+
+
+@pytest.mark.parametrize("case", SWEEP, ids=["s%d_%s_B%d_H%d_dk%d_dv%d_n%d-%d" % c[:8] for c in SWEEP])
+def test_family_sweep_f32_parallel(case):
+    """The same shapes with fp32 q/k/v on the parallel route (the fp32
+    matrix cores; GLA's scores on the vector ALUs with Q~ kept in fp32), at
+    the 1e-5 bar.  Drafts of more than 32 nodes at d_k = 256 do not fit the
+    route's on-chip stage with fp32 activations and are refused there."""
+    _family_sweep_case(case, "parallel", inputs.F32)
+
+
+def _family_sweep_case(case, route, dt):
     i, fam, Bn, H, dk, dv, n0, n1, seed = case
     r = np.random.default_rng(seed)
-    say("family sweep %d %s route %s: B=%d H=%d dk=%d dv=%d n0=%d n1=%d" % (i, fam, route, Bn, H, dk, dv, n0, n1))
-    cfgs = [inputs.Config("fs%d" % k, 700 + 2 * i + k, Bn, H, dk, dv, n, False, n, 64, inputs.BF16, 1)
+    say("family sweep %d %s route %s dtype %s: B=%d H=%d dk=%d dv=%d n0=%d n1=%d"
+        % (i, fam, route, dt, Bn, H, dk, dv, n0, n1))
+    cfgs = [inputs.Config("fs%d" % k, 700 + 2 * i + k, Bn, H, dk, dv, n, False, n, 64, dt, 1)
             for k, n in ((0, n0), (1, n1))]
     drafts = []
     for k, cfg in enumerate(cfgs):
@@ -262,14 +282,21 @@ def test_family_sweep_two_fused_rounds(case, route):
     d0.rnd.path, d0.rnd.length = path, ln
     d0.path, d0.length = _dev(path), _dev(ln)
     S0 = inputs.draw_state(cfgs[0], 0)
-    too_big = fam == "gla" and dk == 256 and max(n0, n1) > 50
+    # beyond the on-chip stage at d_k = 256: the parallel route holds 32 nodes
+    # with GLA's gates or fp32 activations; the serial routes (and AUTO's
+    # fallback to them) 50 nodes with GLA's gates
+    if route == "parallel":
+        limit = 32 if (fam == "gla" or dt == inputs.F32) else 64
+    else:
+        limit = 50 if fam == "gla" else 64
+    too_big = dk == 256 and max(n0, n1) > limit
     f0, f1, g0, g1 = (_factors(c, fam) for c in (cfgs[0], cfgs[1], cfgs[0], cfgs[1]))
     out1, o1 = (torch.empty(Bn, n1, H, dv, device="cuda") for _ in range(2))
     fused = torch.from_numpy(S0).cuda()
     if too_big:
         with pytest.raises(B.SlaError) as e:
-            _verify(cfgs[0] if n0 > 50 else cfgs[1], fam, route, fused, d0 if n0 > 50 else d1,
-                    torch.empty(Bn, max(n0, n1), H, dv, device="cuda"), f0 if n0 > 50 else f1)
+            _verify(cfgs[0] if n0 > limit else cfgs[1], fam, route, fused, d0 if n0 > limit else d1,
+                    torch.empty(Bn, max(n0, n1), H, dv, device="cuda"), f0 if n0 > limit else f1)
         assert e.value.code == B.SLA_ERR_UNSUPPORTED
         return
     _verify(cfgs[0], fam, route, fused, d0, torch.empty(Bn, n0, H, dv, device="cuda"), f0)
@@ -290,4 +317,4 @@ def test_family_sweep_two_fused_rounds(case, route):
     got = out1.cpu().numpy()
     eo = rel_err(np.stack([got[b, :, h] for b, h in units]), _oracle_out(refS, d1, units, fam))
     say("  state err %.2e output err %.2e" % (es, eo))
-    assert es <= TOL[inputs.BF16] and eo <= TOL[inputs.BF16]
+    assert es <= TOL[dt] and eo <= TOL[dt]
