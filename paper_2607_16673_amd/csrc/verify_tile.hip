@@ -52,7 +52,8 @@
 // The tree-masked Grams ([Q; K] K^T tiles that hold ancestor pairs, exact
 // bf16 products) run on the column waves; they and T are done while the
 // first tile's state is still in flight.  Strided global accesses go through
-// buffer descriptors (one VGPR offset per lane).
+// buffer descriptors (one VGPR offset per lane).  With fp32 activations the
+// same structure runs every contraction on the fp32 matrix cores (Layout).
 #include <type_traits>
 
 #include "device.hpp"
@@ -739,8 +740,8 @@ void verify_tile_kernel(VerifyArgs a) {
     }
   }
 
-  // ---- one V-tile: [A] delayed state update, write-back, hi/lo split,
-  //      P = [Q; K] H0 and R on the column waves; barrier (T complete);
+  // ---- one V-tile: [A] delayed state update, write-back, P = [Q; K] H0
+  //      (bf16: state split into hi + lo; fp32: exact) and R on the column waves; barrier (T complete);
   //      [B] U = T R, O = Gamma P_q + Attn U and the stores; then the next
   //      tile's state and values go out.
   const uint32_t obytes = ((uint32_t)(n - 1) * nstride + dv) * 4;
@@ -836,9 +837,10 @@ void verify_tile_kernel(VerifyArgs a) {
           for (int e = 0; e < 8; ++e)
             buf_store_f32<WT ? kPolicyStreamDevice : kPolicyDefault>(hf[ks][e], sr, sv, (uint32_t)(ks * 32 + e) * dv * 4);
       }
-      // P_k = K H0 first (hi/lo split, K-step by K-step as the tile lands),
-      // so that R = beta (v - gamma P_k) takes its place before P_q is built:
-      // the two halves of P are never held at once
+      // P_k = K H0 first (K-step by K-step as the tile lands; bf16: the
+      // state split into hi + lo, fp32: exact products), so that
+      // R = beta (v - gamma P_k) takes its place before P_q is built: the two
+      // halves of P are never held at once
       f32x4 pk[NT];
 #pragma unroll
       for (int mt = 0; mt < NT; ++mt) pk[mt] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -890,26 +892,27 @@ void verify_tile_kernel(VerifyArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) pq[mt] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[e], hf[ks][e], pq[mt], 0, 0, 0);
           }
-      } else
+      } else {
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        bf16x8 bhi, blo;
-        split8(hf[ks], bhi, blo);
+        for (int ks = 0; ks < KS; ++ks) {
+          bf16x8 bhi, blo;
+          split8(hf[ks], bhi, blo);
 #pragma unroll
-        for (int mt = 0; mt < NT; ++mt) {
-          const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
-          pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pq[mt], 0, 0, 0);
-          pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pq[mt], 0, 0, 0);
-          if constexpr (GV) {  // Q~ lo half
-            const bf16x8 afl = *reinterpret_cast<const bf16x8 *>(xl + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
-            pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afl, bhi, pq[mt], 0, 0, 0);
+          for (int mt = 0; mt < NT; ++mt) {
+            const bf16x8 af = *reinterpret_cast<const bf16x8 *>(xs + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
+            pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, bhi, pq[mt], 0, 0, 0);
+            pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, blo, pq[mt], 0, 0, 0);
+            if constexpr (GV) {  // Q~ lo half
+              const bf16x8 afl = *reinterpret_cast<const bf16x8 *>(xl + xchunk<CH>(mt * 16 + lc, ks * 4 + lg));
+              pq[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(afl, bhi, pq[mt], 0, 0, 0);
+            }
           }
         }
       }
     }
     // the next tile's state and values go out now, while this tile's U, O
-    // and stores are computed: its state registers are free since the split,
-    // its values since R
+    // and stores are computed: its state registers are free since P_q, its
+    // values since R
     if (TPW > 1 && more && live(t + 1)) {
       load_state(t + 1, hn, L::kPrefetch ? KS / 2 : 0);
       load_values(t + 1, vraw);
