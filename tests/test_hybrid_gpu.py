@@ -10,7 +10,9 @@ every node, so every level holds many one-node chains), complete binary
 trees, the deepest and widest 64-node drafts, and random trees.  A schedule
 that started a chain before its boundary records existed would read stale
 records and break the equality.  Also: the oracle on sampled units, the
-device data errors, and the factor records."""
+device data errors, the factor records, and the automatic route's choices
+(fp32 drafts on the parallel route, the hybrid fallback for drafts beyond
+the parallel route's on-chip stage)."""
 import numpy as np
 import pytest
 import torch
@@ -164,3 +166,41 @@ def test_hybrid_device_errors_leave_state():
     s = st.cpu().numpy()
     assert s[2] == B.SLA_ERR_PATH and s[0] == 0 and s[1] == 0
     assert torch.equal(state[2], S_before[2])
+
+
+# The automatic route's choices, bit for bit against the explicit route it
+# should take: drafts of two or more nodes go to the parallel route whatever
+# their activation dtype; a draft the parallel route cannot stage on chip
+# (more than 32 nodes at d_k = 256 with fp32 activations or GLA's gates)
+# falls back to the hybrid, which pays for trees of more than 32 nodes.
+ROUTING = [
+    (128, 64, 16, inputs.F32, "gdn", "parallel"),
+    (128, 64, 48, inputs.F32, "decay", "parallel"),
+    (64, 80, 9, inputs.BF16, "deltanet", "parallel"),
+    (256, 48, 48, inputs.F32, "gdn", "hybrid"),
+    (256, 32, 40, inputs.BF16, "gla", "hybrid"),
+    (256, 48, 64, inputs.F32, "deltanet", "hybrid"),
+]
+
+
+@pytest.mark.parametrize("dk,dv,n,dt,fam,expect", ROUTING,
+                         ids=["dk%d_dv%d_n%d_%s_%s_%s" % c for c in ROUTING])
+def test_automatic_route_choices(dk, dv, n, dt, fam, expect):
+    r = np.random.default_rng(dk + 7 * n + len(fam))
+    Bn, H = 4, 2
+    parents0 = [inputs.random_tree(r, n, max(2, min(n, 8)), 4) for _ in range(Bn)]
+    parents1 = [inputs.random_tree(r, n, max(2, min(n, 8)), 4) for _ in range(Bn)]
+    cfg, r0, a0, b0, S0 = _problem(31 + n, Bn, H, dk, dv, n, parents0, dt, fam)
+    _, r1, a1, b1, _ = _problem(32 + n, Bn, H, dk, dv, n, parents1, dt, fam)
+    say("automatic route dk=%d dv=%d n=%d %s %s: expect %s" % (dk, dv, n, dt, fam, expect))
+    s_auto, res_auto = _two_rounds(cfg, r0, a0, b0, r1, a1, b1, S0, fam, "auto")
+    s_exp, res_exp = _two_rounds(cfg, r0, a0, b0, r1, a1, b1, S0, fam, expect)
+    assert torch.equal(s_auto, s_exp)
+    for (o_a, f_a), (o_e, f_e) in zip(res_auto, res_exp):
+        assert torch.equal(o_a, o_e)
+        assert torch.equal(f_a.u, f_e.u) and torch.equal(f_a.k, f_e.k)
+    ref, st = oracle.verify(S0, r0.q32[0], r0.k32[0], r0.v32[0], a0, b0, r0.parent, family=fam)
+    assert (st == 0).all()
+    err = rel_err(res_auto[0][0].cpu().numpy(), ref)
+    say("  round 0 output rel err %.3e" % err)
+    assert err <= TOL[dt]
