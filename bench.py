@@ -179,7 +179,7 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on exactly one GPU: this build has no multi-GPU path "
+        print("bench.py runs on exactly one GPU: the library has no multi-GPU path "
               "(every (batch, head) unit is independent: a sharded run would give each GPU whole sequences "
               "or a share of the heads, with no exchange inside verification or commit).",
               file=sys.stderr)

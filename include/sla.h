@@ -52,7 +52,7 @@ extern "C" {
 #define SLA_ERR_TOPOLOGY (-4)    /* parent array not in topological order  */
 #define SLA_ERR_PATH (-5)        /* accepted path is not a root path       */
 #define SLA_ERR_ALIAS (-6)       /* pending factors overlap output factors */
-#define SLA_ERR_UNSUPPORTED (-7) /* valid request this build cannot run    */
+#define SLA_ERR_UNSUPPORTED (-7) /* valid request the library cannot run  */
 #define SLA_ERR_HIP (-8)         /* the HIP runtime reported an error      */
 #define SLA_ERR_SCORE (-9)       /* a draft log-probability above 0 or NaN */
 
